@@ -1,0 +1,138 @@
+"""Pins of the oracle's generator against independent implementations and statistics."""
+
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.philox import philox4
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.mark.parametrize("key", [(0, 0), (5, 7), (2 ** 64 - 1, 12345), (0x0123456789ABCDEF, 0xFEDCBA9876543210)])
+@pytest.mark.parametrize("start", [(0, 0, 0, 0), (3, 0, 0, 0), (2 ** 64 - 3, 0, 9, 1), (11, 2 ** 63, 2 ** 40, 2 ** 64 - 1)])
+def test_philox4x64_10_matches_numpy(key, start):
+    """numpy.random.Philox is Philox4x64-10; it increments the 256-bit counter before each block."""
+    n_blocks = 6
+    g = np.random.Philox(key=np.array(key, dtype=np.uint64), counter=np.array(start, dtype=np.uint64))
+    raw = g.random_raw(4 * n_blocks)
+    c = sum(int(w) << (64 * i) for i, w in enumerate(start))
+    ctrs = [(c + 1 + b) % 2 ** 256 for b in range(n_blocks)]
+    words = [[(x >> (64 * i)) & (2 ** 64 - 1) for x in ctrs] for i in range(4)]
+    out = philox4([np.array(w, dtype=np.uint64) for w in words], key, width=64, rounds=10)
+    mine = np.stack(out, axis=1).reshape(-1)
+    np.testing.assert_array_equal(mine, raw)
+
+
+def test_philox4x64_round_count_matters():
+    """A wrong round count must not pass the numpy pin."""
+    g = np.random.Philox(key=[1, 2], counter=[0, 0, 0, 0])
+    raw = g.random_raw(4)
+    out = philox4([np.uint64(1), np.uint64(0), np.uint64(0), np.uint64(0)], (1, 2), width=64, rounds=9)
+    assert not np.array_equal(np.array([int(w) for w in out], dtype=np.uint64), raw)
+
+
+@pytest.fixture(scope="session")
+def rocrand_ref(tmp_path_factory):
+    src = os.path.join(HERE, "helpers", "rocrand_philox_ref.cpp")
+    if shutil.which("g++") is None or not os.path.exists("/opt/rocm/include/rocrand/rocrand_philox4x32_10.h"):
+        pytest.skip("g++ or rocRAND headers not available")
+    exe = str(tmp_path_factory.mktemp("rr") / "rr")
+    subprocess.run(["g++", "-O1", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", src, "-o", exe],
+                   check=True, capture_output=True)
+    return exe
+
+
+def test_philox4x32_10_matches_rocrand(rocrand_ref):
+    """rocRAND's Philox4x32-10 engine (open source, compiled here for the host) agrees bit for bit."""
+    rng = np.random.default_rng(42)
+    cases = [(0, 0, 0, 0), (1, 0, 0, 0), (2 ** 64 - 1, 2 ** 32 - 1, 2 ** 32 - 1, 2 ** 29 - 1),
+             (0xDEADBEEF, 2 ** 32, 7, 3), (12345, 1_873_342_080, 0, 1)]
+    for _ in range(200):
+        cases.append((int(rng.integers(0, 2 ** 63)) * 2 + int(rng.integers(0, 2)),
+                      int(rng.integers(0, 2 ** 36)), int(rng.integers(0, 2 ** 32)), int(rng.integers(0, 2 ** 29))))
+    inp = "".join(f"{s} {t} {st} {g}\n" for s, t, st, g in cases)
+    out = subprocess.run([rocrand_ref], input=inp, capture_output=True, text=True, check=True).stdout.split("\n")
+    for (s, t, st, g), line in zip(cases, out):
+        ref = [int(v) for v in line.split()]
+        mine = [int(w[0]) for w in oracle.tile_words([t], s, st, g)]
+        assert mine == ref, (s, t, st, g)
+
+
+def test_philox4x32_scalar_bigint():
+    """Vectorised uint64 arithmetic agrees with Python big integers near word overflow."""
+    M0, M1, W0, W1 = 0xD2511F53, 0xCD9E8D57, 0x9E3779B9, 0xBB67AE85
+    m = 2 ** 32 - 1
+
+    def ref(c, k):
+        c, k = list(c), list(k)
+        for _ in range(10):
+            p0, p1 = M0 * c[0], M1 * c[2]
+            c = [(p1 >> 32) ^ c[1] ^ k[0], p1 & m, (p0 >> 32) ^ c[3] ^ k[1], p0 & m]
+            k = [(k[0] + W0) & m, (k[1] + W1) & m]
+        return c
+
+    for c in [(m, m, m, m), (0, 0, 0, 0), (m, 0, m, 0), (123456789, 987654321, 55, 66)]:
+        for k in [(m, m), (0, 0), (0x12345678, 0x9ABCDEF0)]:
+            out = philox4([np.uint64(v) for v in c], k, width=32, rounds=10)
+            assert [int(v) for v in out] == ref(c, k)
+
+
+def test_bit_balance_and_independence():
+    """Probe bits are balanced per bit position and uncorrelated across groups, steps and tiles."""
+    n_tiles = 1 << 16
+    a = oracle.tile_bytes(0, n_tiles, 7, 3, 0)
+    b = oracle.tile_bytes(0, n_tiles, 7, 3, 1)
+    c = oracle.tile_bytes(0, n_tiles, 7, 4, 0)
+    d = oracle.tile_bytes(1, n_tiles, 7, 3, 0)
+    bits = lambda x: np.unpackbits(x.reshape(-1)[:, None], axis=1, bitorder="little")  # [bytes, 8]
+    A = bits(a)
+    n = A.shape[0]
+    # per probe bit: fraction of ones within 5 sigma of 1/2
+    frac = A.mean(axis=0)
+    assert np.all(np.abs(frac - 0.5) < 5 * 0.5 / np.sqrt(n)), frac
+    # correlation between sign vectors of different groups / steps / shifted tiles
+    sa = 2.0 * A - 1.0
+    for other in (b, c, d):
+        so = 2.0 * bits(other) - 1.0
+        corr = (sa * so).mean(axis=0)
+        assert np.all(np.abs(corr) < 5 / np.sqrt(n)), corr
+    # correlation between probe bits within one byte
+    cc = (sa.T @ sa) / n
+    off = cc[~np.eye(8, dtype=bool)]
+    assert np.all(np.abs(off) < 5 / np.sqrt(n)), off
+
+
+def test_tile_layout_byte_order():
+    """Element i's byte is byte (i mod 4) of word (i mod 16) // 4 of its tile's block."""
+    t0, nt = 5, 3
+    words = oracle.tile_words(np.arange(t0, t0 + nt), 99, 1, 2)
+    tb = oracle.tile_bytes(t0, nt, 99, 1, 2)
+    eb = oracle.element_bytes(16 * t0, 16 * nt, 99, 1, 2)
+    for t in range(nt):
+        for j in range(16):
+            expect = (int(words[j // 4][t]) >> (8 * (j % 4))) & 0xFF
+            assert tb[t, j] == expect
+            assert eb[16 * t + j] == expect
+
+
+def test_signs_window_consistency():
+    """Any window (unaligned offset, ragged tail) reads the same global probe values."""
+    full = oracle.signs(0, 4096, 3, 9, 13)
+    for off, n in [(0, 1), (1, 15), (7, 33), (16, 16), (4095, 1), (100, 3000)]:
+        np.testing.assert_array_equal(oracle.signs(off, n, 3, 9, 13), full[off:off + n])
+    far = 2 ** 35 + 5
+    np.testing.assert_array_equal(oracle.signs(far + 10, 20, 3, 9, 13), oracle.signs(far, 40, 3, 9, 13)[10:30])
+
+
+def test_sign_convention_set_bit_is_plus_one():
+    """Appendix F's convention: a set bit selects +1, a clear bit -1; probe k uses bit k mod 8."""
+    eb = oracle.element_bytes(0, 256, 1, 0, 1)
+    for k in range(8, 16):
+        s = oracle.signs(0, 256, 1, 0, k)
+        bit = (eb >> (k - 8)) & 1
+        assert np.all((s == 1) == (bit == 1))
