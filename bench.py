@@ -1,0 +1,178 @@
+"""Benchmark: one 1.5-SPSA step of probe regenerate-and-apply sweeps on one MI355X.
+
+A step is Algorithm 1 on one device with the forward passes replaced by synthetic losses:
+for each of K probes zo_perturb(+eps), zo_perturb(-2 eps), zo_perturb(+eps); then
+zo_probe_coeffs on the host; then one fused zo_update. Weights are one flat bf16 buffer
+shaped like OPT-13B (12,853,473,280 parameters, ~N(0, 0.02)), resident in HBM before the
+timed region starts; K = 16, eps = lr = 1e-3.
+
+Prints one JSON line. `value` is the step's effective HBM bandwidth: algorithmic bytes
+(one read and one write of every weight per sweep, 3K + 1 sweeps) over the step time.
+Per-kernel durations come from HIP events recorded around every launch on the stream the
+kernels run on; `roofline` is the dominant kernel's (zo_perturb: 3K of the 3K + 1 sweeps)
+and `roofline_update` the fused update's.
+"""
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused probe-update effective HBM GB/s + params·probes/s (OPT-13B shape, K=16)"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, K, budget_s=15.0):
+    """The oracle on the host: one step (3K perturbs + one update) over a window of the workload."""
+    import numpy as np
+
+    import oracle
+    import workloads
+
+    m = 1 << 16
+    th = workloads.normal_bf16_bits(m, 0)
+    lp, lm, l0 = workloads.synthetic_losses(K, 0)
+    windows, t_total, sweeps = 0, 0.0, 0
+    rng = np.random.default_rng(1)
+    while t_total < budget_s and windows < 64:
+        off = int(rng.integers(0, w.n - m))
+        t0 = time.perf_counter()
+        oracle.full_step(th, w.dtype, off, 2024, 0, w.eps, w.lr, lp, lm, l0)
+        t_total += time.perf_counter() - t0
+        windows += 1
+        sweeps += 3 * K + 1
+    b = 2 if w.dtype == "bf16" else 4
+    gbps = sweeps * 2 * b * m / t_total / 1e9
+    return {"value": round(gbps, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{windows} full steps (3K+1 = {3 * K + 1} sweeps) over windows of {m} weights at random "
+                      f"offsets of the {w.name} buffer, single-threaded numpy, {t_total:.1f} s; "
+                      f"host {platform.processor() or platform.machine()}, os.cpu_count()={os.cpu_count()}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="opt13b", help="tiny, opt125m, opt1.3b, opt13b or opt30b")
+    ap.add_argument("--K", type=int, default=0, help="probes per step (default: the workload's first)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_38095_amd as zo
+    import workloads
+
+    w = workloads.WORKLOADS[args.workload]
+    K = args.K or w.K[0]
+    n, b = w.n, (2 if w.dtype == "bf16" else 4)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda:0")
+    zo.library()
+    log(f"workload {w.name}: n={n} dtype={w.dtype} K={K} eps={w.eps} lr={w.lr}; {n * b / 1e9:.2f} GB of weights")
+
+    theta = torch.empty(n, dtype=dt, device=dev)
+    if w.hidden:
+        workloads.fill_opt_buffer_device(theta, w)
+    else:
+        theta.copy_(torch.from_numpy(workloads.tiny_theta(n)))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    seed = 2024
+
+    ev = {"perturb": [], "update": []}
+
+    def timed(kind, fn):
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        z.record(stream)
+        ev[kind].append((a, z))
+
+    def one_step(step, record):
+        lp, lm, l0 = workloads.synthetic_losses(K, step)
+        for k in range(K):
+            for e in (w.eps, -2.0 * w.eps, w.eps):
+                if record:
+                    timed("perturb", lambda: zo.zo_perturb(theta, k, e, seed, step, stream=stream))
+                else:
+                    zo.zo_perturb(theta, k, e, seed, step, stream=stream)
+        c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
+        if record:
+            timed("update", lambda: zo.zo_update(theta, c, w.lr, seed, step, stream=stream))
+        else:
+            zo.zo_update(theta, c, w.lr, seed, step, stream=stream)
+
+    for s in range(args.warmup):
+        one_step(s, False)
+        torch.cuda.synchronize()
+        log(f"warmup step {s} done")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        one_step(args.warmup + s, True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log(f"timed {args.steps} steps in {elapsed:.3f} s")
+
+    ms = {k: np.array([a.elapsed_time(z) for a, z in v]) for k, v in ev.items()}
+    t_step = elapsed / args.steps
+    sweep_bytes = 2.0 * b * n
+    step_bytes = (3 * K + 1) * sweep_bytes
+    gbps = step_bytes / t_step / 1e9
+    p_ms, u_ms = float(ms["perturb"].mean()), float(ms["update"].mean())
+    p_gbps, u_gbps = sweep_bytes / (p_ms * 1e-3) / 1e9, sweep_bytes / (u_ms * 1e-3) / 1e9
+
+    def roof(kernel, avg_ms, gb):
+        return {"kernel": kernel, "bound": "hbm", "achieved": round(gb, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(gb / HBM_PEAK_GBPS, 4), "traffic": None, "avg_ms": round(avg_ms, 4),
+                "bytes_per_launch": sweep_bytes}
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbps, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded OPT-shaped weights ~N(0,0.02), losses ~N(2.0,0.05))",
+        "config": {"workload": f"{w.name}-shaped flat {w.dtype} parameter set, full 1.5-SPSA step",
+                   "n_params": n, "K": K, "eps": w.eps, "lr": w.lr, "sweeps_per_step": 3 * K + 1,
+                   "parallelism": "single GPU"},
+        "update_gbps": round(u_gbps, 1),
+        "update_params_probes_per_s": float(f"{n * K / (u_ms * 1e-3):.4e}"),
+        "perturb_gbps": round(p_gbps, 1),
+        "step_params_probes_per_s": float(f"{n * 4 * K / t_step:.4e}"),
+        "roofline": roof("zo_perturb", p_ms, p_gbps),
+        "roofline_update": roof("zo_update", u_ms, u_gbps),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline(w, K)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

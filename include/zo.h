@@ -1,0 +1,144 @@
+/*
+ * zo.h -- C ABI of libzo: the probe regenerate-and-apply sweep of 1.5-SPSA on gfx950.
+ *
+ * 1.5-SPSA ("Probe-Space Preconditioning for Fast and Stable Zero-Order Training")
+ * estimates a descent direction from antithetic loss pairs L(theta +- eps z_k) along
+ * Rademacher probes z_k plus one clean loss L(theta), and weights each probe by its
+ * measured curvature (section 4.1, Eq. 3 and 4; section 4.2, Eq. 5 and 6; Algorithm 1).
+ * The probes are never stored: every sweep regenerates z_k from (seed, step, k, element
+ * index) with a counter-based generator, 8 probe signs per byte (section 4.3).
+ *
+ * Probe definition (shared by every call below):
+ *   element i (a 64-bit global index) belongs to tile t = i / 16; probe k belongs to
+ *   group g = k / 8. The tile's block is Philox4x32-10 (Salmon et al., SC'11) with
+ *   counter (t mod 2^32, t / 2^32, step, g) and key (seed mod 2^32, seed / 2^32), four
+ *   32-bit words x0..x3. Element i's byte is byte (i mod 4) of word x_((i mod 16) / 4);
+ *   z_k[i] = +1 if bit (k mod 8) of that byte is set, else -1 (appendix F's convention).
+ *
+ * Conventions for every call:
+ *   - params: caller-owned device memory, a contiguous flat array of n elements of the
+ *     given dtype, aligned to the element size. The library never allocates, frees or
+ *     retains it; it must stay valid until the stream work has finished.
+ *   - offset: the global element index of params[0], so a shard or window of a larger
+ *     parameter vector regenerates the same probe values as the whole vector would.
+ *     offset + n must not exceed 2^64.
+ *   - stream: a hipStream_t (NULL = the default stream). Device work is enqueued on it
+ *     and the call returns without waiting; faults surface at the caller's next
+ *     synchronisation. Host arguments (coefficient arrays) are copied before return.
+ *   - Errors: every argument is validated before anything is launched; on a negative
+ *     status nothing was enqueued and no output was written. n = 0 (or K = 0) is a
+ *     successful no-op.
+ *   - No global state is kept between calls except an optional launch-width override
+ *     (zo_set_max_blocks); calls on different streams may run concurrently on disjoint
+ *     parameter memory.
+ */
+#ifndef ZO_H_
+#define ZO_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { ZO_F32 = 0, ZO_BF16 = 1 } zo_dtype;
+
+enum {
+  ZO_OK = 0,
+  ZO_ERR_NULL = -1,      /* a required pointer is NULL */
+  ZO_ERR_ARG = -2,       /* bad dtype, misalignment, K out of range, index overflow */
+  ZO_ERR_NONFINITE = -3, /* a non-finite eps, lr, loss or coefficient */
+  ZO_ERR_HIP = -4        /* the HIP runtime refused the launch */
+};
+
+/* Most probes one zo_update call applies (coefficients travel as kernel arguments). */
+#define ZO_K_MAX 256u
+
+/*
+ * zo_perturb -- theta[i] <- theta[i] + eps * z_k[offset + i], for i in [0, n).
+ * Algorithm 1 applies each probe three times around its two perturbed forward passes,
+ * with eps = +e, then -2e, then +e (restoring theta up to rounding).
+ * Arithmetic: one IEEE fp32 addition (bf16 weights widened exactly, the sum rounded back
+ * to bf16 to nearest-even). The result is bit-exact and independent of launch shape.
+ * Errors: ZO_ERR_NULL (params NULL with n > 0), ZO_ERR_ARG (dtype, alignment, index
+ * overflow), ZO_ERR_NONFINITE (eps), ZO_ERR_HIP.
+ */
+int zo_perturb(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
+               uint32_t step, uint32_t k, float eps, void* stream);
+
+/*
+ * zo_probe_coeffs -- host function: per-probe update coefficients c[K] from the losses.
+ *   curvature (section 4.1, Eq. 3):   chat_k = (L_plus[k] - 2 L_clean + L_minus[k]) / eps^2
+ *   weight    (section 4.1, Eq. 4):   w_k = 1 / max(lambda_reg, |chat_k|^alpha)
+ *   coefficient (Eq. 5/6, Alg. 1):    c_k = w_k (L_plus[k] - L_minus[k]) / (2 K eps)
+ * so that zo_update with lr = eps applies Algorithm 1's gamma_k = (1/2n)(L+ - L-) w_k.
+ * zo_probe_coeffs uses the paper's alpha = 0.1 and lambda_reg = 1.
+ * Arithmetic is IEEE float64 in exactly this order: d2 = (L+ - 2*L0) + L-;
+ * chat = d2/(eps*eps); a = pow(|chat|, alpha); den = a > lambda_reg ? a : lambda_reg;
+ * w = 1/den; c64 = ((L+ - L-)*w)/((2*K)*eps); c = (float)c64 (nearest-even).
+ * Inputs are host arrays of K doubles; outputs are host arrays of K entries, each
+ * optional (NULL) in the _ex form. Never touches the GPU.
+ * Errors: ZO_ERR_NULL (loss arrays or c_out NULL), ZO_ERR_ARG (K = 0, eps <= 0,
+ * alpha outside [0, 1], lambda_reg <= 0), ZO_ERR_NONFINITE (any non-finite input).
+ * Outputs are written only on success.
+ */
+int zo_probe_coeffs(const double* L_plus, const double* L_minus, uint32_t K, double L_clean,
+                    double eps, float* c_out);
+int zo_probe_coeffs_ex(const double* L_plus, const double* L_minus, uint32_t K, double L_clean,
+                       double eps, double alpha, double lambda_reg, float* c_out,
+                       double* c64_out, double* curv_out, double* w_out);
+
+/*
+ * zo_update -- theta[i] <- theta[i] - lr * sum_{k<K} c[k] z_k[i], for global i in [0, n).
+ * The fused form of section 4.2 (Eq. 6, Delta theta = -eta Z W Delta l) and of
+ * Algorithm 1's per-probe loop: one read and one write of theta for all K probes, which
+ * are regenerated in registers. c: host array of K floats (from zo_probe_coeffs).
+ * Arithmetic: per element, sum_k c[k] z_k in fp32 (pairwise over each group of 8 probes,
+ * pairwise or compensated across groups), s = fl(lr * sum), theta - s in fp32, then one
+ * rounding to bf16 for bf16 weights. With K = 1 this equals zo_perturb(k = 0,
+ * eps = -fl(lr * c[0])) bit for bit.
+ * Errors: ZO_ERR_NULL (params NULL with n > 0, c NULL with K > 0), ZO_ERR_ARG (dtype,
+ * alignment, K > ZO_K_MAX, k_base + K > 2^32), ZO_ERR_NONFINITE (lr or any c[k]), ZO_ERR_HIP.
+ */
+int zo_update(void* params, zo_dtype dtype, uint64_t n, uint64_t seed, uint32_t step,
+              uint32_t K, const float* c, float lr, void* stream);
+
+/*
+ * zo_update_ex -- zo_update over global elements [offset, offset + n) for probes
+ * k_base .. k_base + K - 1 (c[j] belongs to probe k_base + j). A shard of a larger
+ * vector passes its offset; more than ZO_K_MAX probes are applied as several calls with
+ * increasing k_base (each call rounds theta once).
+ */
+int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
+                 uint32_t step, uint32_t k_base, uint32_t K, const float* c, float lr,
+                 void* stream);
+
+/*
+ * zo_gen_bits -- writes the raw 16-byte probe block of each tile tile_begin ..
+ * tile_begin + n_tiles - 1 for probe group `group` (probes 8*group .. 8*group+7) to
+ * out_dev (device memory, 16 * n_tiles bytes, caller-owned). Exposes the generator for
+ * bit-exact checks; the sweeps never store probes.
+ * Errors: ZO_ERR_NULL (out_dev NULL with n_tiles > 0), ZO_ERR_ARG (tile index overflow
+ * past 2^60), ZO_ERR_HIP.
+ */
+int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_t seed,
+                uint32_t step, uint32_t group, void* stream);
+
+/* zo_strerror -- static description of a status code. */
+const char* zo_strerror(int status);
+
+/*
+ * zo_set_max_blocks -- caps the number of workgroups per sweep launch (0 restores the
+ * default). Results do not depend on it; it exists to check that and to tune launch
+ * width. Process-wide; not synchronised with launches in flight on other threads.
+ */
+void zo_set_max_blocks(uint32_t max_blocks);
+
+/* zo_version -- library version string. */
+const char* zo_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZO_H_ */

@@ -1,0 +1,309 @@
+"""GPU parity: libzo's kernels against the CPU oracle on the same seeded inputs.
+
+Bars: generated probe bits and perturb results bit-exact; update within
+|gpu - oracle| <= 1e-6 * max(|theta|, lr * sum_k |c_k|) for fp32 weights, and for bf16
+weights within one bf16 ulp of the result plus that same fp32 allowance (the kernel forms
+theta - lr * sum in fp32 before its single rounding to bf16, so where the result cancels
+to nearly zero the fp32 rounding of the operands can exceed a bf16 ulp of the result);
+coefficients bit-exact (host tests).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_38095_amd as zo
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def note(msg):
+    print(msg, flush=True)
+
+
+def to_dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def to_dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def host_bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def bf16_spacing(x):
+    m = np.abs(x)
+    e = np.floor(np.log2(np.maximum(m, 2.0 ** -126)))
+    return np.where(m < 2.0 ** -126, 2.0 ** -133, 2.0 ** (e - 7))
+
+
+def assert_bf16_within_1ulp(got_bits, want_bits, theta_bits=None, c=(), lr=0.0):
+    g = oracle.bf16_to_f64(got_bits)
+    w = oracle.bf16_to_f64(want_bits)
+    err = np.abs(g - w)
+    allow = bf16_spacing(np.maximum(np.abs(g), np.abs(w)))
+    if theta_bits is not None:
+        scale = np.maximum(np.abs(oracle.bf16_to_f64(theta_bits)), abs(lr) * np.abs(np.asarray(c, np.float64)).sum())
+        allow = allow + 1e-6 * scale
+    ok = err <= allow
+    assert np.all(ok), f"{np.count_nonzero(~ok)} elements beyond 1 bf16 ulp; first at {np.argmax(~ok)}"
+    return np.count_nonzero(got_bits != want_bits)
+
+
+def assert_f32_update_close(got, want, c, lr):
+    scale = np.maximum(np.abs(want.astype(np.float64)), abs(lr) * np.abs(np.asarray(c, np.float64)).sum())
+    err = np.abs(got.astype(np.float64) - want.astype(np.float64))
+    ok = err <= 1e-6 * scale
+    assert np.all(ok), f"max rel err {np.max(err / scale):.3e}"
+    return float(np.max(err / scale))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    zo.library()
+    zo.zo_set_max_blocks(0)
+    yield
+    zo.zo_set_max_blocks(0)
+
+
+# ----------------------------------------------------------------------------- generator
+@pytest.mark.parametrize("tile_begin,n_tiles,seed,step,group", [
+    (0, 1, 0, 0, 0),
+    (0, 4096, 1, 0, 0),
+    (12345, 777, 2 ** 64 - 1, 2 ** 32 - 1, 3),
+    (2 ** 32 - 5, 20, 0xDEADBEEFCAFEF00D, 7, 2 ** 29 - 1),   # counter word 0 wraps into word 1
+    (1_873_342_080, 1000, 42, 1, 1),                         # OPT-30B's last tiles
+])
+def test_gen_bits_bit_exact(tile_begin, n_tiles, seed, step, group):
+    note(f"gen_bits tiles [{tile_begin}, +{n_tiles}) seed {seed} step {step} group {group}")
+    out = torch.zeros(16 * n_tiles, dtype=torch.uint8, device=DEV)
+    zo.zo_gen_bits(out, tile_begin, seed, step, group)
+    got = out.cpu().numpy().reshape(n_tiles, 16)
+    np.testing.assert_array_equal(got, oracle.tile_bytes(tile_begin, n_tiles, seed, step, group))
+
+
+# ----------------------------------------------------------------------------- perturb
+PERTURB_CASES = [
+    # n, offset, k, eps
+    (1, 0, 0, 1e-3), (15, 0, 1, 1e-3), (16, 0, 7, -2e-3), (17, 0, 8, 1e-3), (1000, 3, 63, 1e-4),
+    (65_536 + 13, 0, 1000, 1e-3), (4099, 2 ** 35 + 7, 5, -2e-3), (300_000, 16, 17, 1e-3),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,offset,k,eps", PERTURB_CASES)
+def test_perturb_bit_exact(dtype, n, offset, k, eps):
+    note(f"perturb {dtype} n {n} offset {offset} k {k} eps {eps}")
+    seed, step = 1234567, 3
+    if dtype == "f32":
+        th = workloads.normal_f32(n, n)
+        t = to_dev_f32(th)
+        zo.zo_perturb(t, k, eps, seed, step, offset=offset)
+        np.testing.assert_array_equal(t.cpu().numpy(), oracle.perturb(th, "f32", offset, seed, step, k, eps))
+    else:
+        th = workloads.normal_bf16_bits(n, n)
+        t = to_dev_bf16(th)
+        zo.zo_perturb(t, k, eps, seed, step, offset=offset)
+        np.testing.assert_array_equal(host_bits(t), oracle.perturb(th, "bf16", offset, seed, step, k, eps))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shift,offset", [(1, 1), (1, 0), (3, 0), (5, 12)])
+def test_perturb_unaligned_storage(dtype, shift, offset):
+    """A view starting mid-tile: vector path when (pointer, offset) agree, element path otherwise."""
+    note(f"perturb unaligned {dtype} shift {shift} offset {offset}")
+    n = 5000
+    if dtype == "f32":
+        th = workloads.normal_f32(n + shift, 5)
+        t = to_dev_f32(th)
+        zo.zo_perturb(t[shift:], 9, 1e-3, 1, 2, offset=offset)
+        want = th.copy()
+        want[shift:] = oracle.perturb(th[shift:], "f32", offset, 1, 2, 9, 1e-3)
+        np.testing.assert_array_equal(t.cpu().numpy(), want)
+    else:
+        th = workloads.normal_bf16_bits(n + shift, 5)
+        t = to_dev_bf16(th)
+        zo.zo_perturb(t[shift:], 9, 1e-3, 1, 2, offset=offset)
+        want = th.copy()
+        want[shift:] = oracle.perturb(th[shift:], "bf16", offset, 1, 2, 9, 1e-3)
+        np.testing.assert_array_equal(host_bits(t), want)
+
+
+def test_perturb_bf16_rounding_ties_and_subnormals():
+    """Crafted exact ties of the fp32 sum (both parities) and subnormal bf16 weights."""
+    vals = []
+    for m in range(128):
+        vals += [1.0 + m * 2.0 ** -7, -(1.0 + m * 2.0 ** -7), 0.5 + m * 2.0 ** -8]
+    th = oracle.f32_to_bf16(np.array(vals, np.float32))
+    sub = np.arange(1, 200, dtype=np.uint16)  # positive bf16 subnormals
+    th = np.concatenate([th, sub, sub | np.uint16(0x8000), np.zeros(7, np.uint16)])
+    for eps in (2.0 ** -8, 2.0 ** -9, 3 * 2.0 ** -130, 1e-3):
+        t = to_dev_bf16(th)
+        zo.zo_perturb(t, 3, eps, 77, 0)
+        np.testing.assert_array_equal(host_bits(t), oracle.perturb(th, "bf16", 0, 77, 0, 3, eps))
+
+
+def test_perturb_schedule_restores_fp32_within_1ulp():
+    """Algorithm 1's +eps, -2 eps, +eps on the tiny workload: within 1 ulp of the largest intermediate."""
+    th = workloads.tiny_theta()
+    t = to_dev_f32(th)
+    mags = [np.abs(th)]
+    for e in (1e-3, -2e-3, 1e-3):
+        zo.zo_perturb(t, 2, e, 0, 0)
+        mags.append(np.abs(t.cpu().numpy()))
+    got = t.cpu().numpy()
+    M = np.maximum.reduce(mags)
+    assert np.all(np.abs(got.astype(np.float64) - th) <= np.spacing(M).astype(np.float64))
+
+
+# ----------------------------------------------------------------------------- update
+UPDATE_CASES = [
+    # n, offset, k_base, K
+    (1000, 0, 0, 1), (4096, 0, 0, 4), (4097, 0, 0, 8), (3333, 5, 0, 9), (70_001, 0, 0, 16),
+    (20_000, 2 ** 33 + 1, 0, 24), (20_000, 0, 0, 32), (50_000, 0, 0, 64), (9_000, 0, 0, 65),
+    (5_000, 0, 0, 200), (3_000, 0, 0, 256), (10_000, 48, 3, 16), (10_000, 0, 8, 16), (7_000, 0, 100, 57),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,offset,k_base,K", UPDATE_CASES)
+def test_update_matches_oracle(dtype, n, offset, k_base, K):
+    note(f"update {dtype} n {n} offset {offset} k_base {k_base} K {K}")
+    seed, step, lr = 99, 5, 1e-3
+    c = np.random.default_rng(K).standard_normal(K).astype(np.float32) * 3
+    if dtype == "f32":
+        th = workloads.normal_f32(n, 1)
+        t = to_dev_f32(th)
+        zo.zo_update_ex(t, c, lr, seed, step, offset=offset, k_base=k_base)
+        want = oracle.update(th, "f32", offset, seed, step, c, lr, k_base=k_base)
+        assert_f32_update_close(t.cpu().numpy(), want, c, lr)
+    else:
+        th = workloads.normal_bf16_bits(n, 1)
+        t = to_dev_bf16(th)
+        zo.zo_update_ex(t, c, lr, seed, step, offset=offset, k_base=k_base)
+        want = oracle.update(th, "bf16", offset, seed, step, c, lr, k_base=k_base)
+        assert_bf16_within_1ulp(host_bits(t), want, th, c, lr)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_update_k1_equals_perturb(dtype):
+    n, c0, lr = 100_003, np.float32(0.7310586), np.float32(1e-3)
+    base = workloads.normal_f32(n, 8)
+    if dtype == "f32":
+        a, b = to_dev_f32(base), to_dev_f32(base)
+    else:
+        bits = oracle.f32_to_bf16(base)
+        a, b = to_dev_bf16(bits), to_dev_bf16(bits)
+    zo.zo_update(a, [c0], lr, 4, 2)
+    zo.zo_perturb(b, 0, -(lr * c0), 4, 2)
+    assert torch.equal(a.view(torch.int16) if dtype == "bf16" else a, b.view(torch.int16) if dtype == "bf16" else b)
+
+
+@pytest.mark.parametrize("op", ["perturb", "update16", "update64", "update200"])
+def test_results_independent_of_grid(op):
+    n = 1_000_003
+    th = workloads.normal_bf16_bits(n, 3)
+    c = np.random.default_rng(0).standard_normal(256).astype(np.float32)
+    outs = []
+    for blocks in (1, 7, 64, 0):
+        zo.zo_set_max_blocks(blocks)
+        t = to_dev_bf16(th)
+        if op == "perturb":
+            zo.zo_perturb(t, 11, 1e-3, 5, 1)
+        else:
+            K = int(op[6:])
+            zo.zo_update(t, c[:K], 1e-3, 5, 1)
+        outs.append(host_bits(t))
+    zo.zo_set_max_blocks(0)
+    for o in outs[1:]:
+        np.testing.assert_array_equal(o, outs[0])
+
+
+def test_update_linearity_fp32():
+    th = workloads.normal_f32(200_000, 4)
+    c = np.random.default_rng(9).standard_normal(16).astype(np.float32)
+    t = to_dev_f32(th)
+    zo.zo_update(t, c, 1e-3, 1, 1)
+    mid = np.abs(t.cpu().numpy())
+    zo.zo_update(t, -c, 1e-3, 1, 1)
+    got = t.cpu().numpy().astype(np.float64)
+    M = np.maximum(np.abs(th), mid)
+    assert np.all(np.abs(got - th) <= 2 * np.spacing(M).astype(np.float64))
+
+
+def test_empty_and_noop_calls():
+    t = torch.zeros(0, dtype=torch.float32, device=DEV)
+    zo.zo_perturb(t, 0, 1e-3, 0, 0)
+    zo.zo_update(t, [1.0], 1e-3, 0, 0)
+    u = to_dev_f32(workloads.normal_f32(100, 0))
+    before = u.clone()
+    zo.zo_update(u, [], 1e-3, 0, 0)
+    assert torch.equal(u, before)
+    with pytest.raises(zo.ZoError):
+        zo.zo_update(u, np.zeros(zo.ZO_K_MAX + 1, np.float32), 1e-3, 0, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(u, before)
+
+
+# ----------------------------------------------------------------------------- full step
+def test_full_tiny_step():
+    """The tiny fp32 workload: 2^20 weights, K = 4, eps 1e-3, lr 1e-4 (schedule + coeffs + update)."""
+    w = workloads.WORKLOADS["tiny"]
+    K = w.K[0]
+    th = workloads.tiny_theta(w.n)
+    lp, lm, l0 = workloads.synthetic_losses(K, 1)
+    t = to_dev_f32(th)
+    for k in range(K):
+        for e in (w.eps, -2 * w.eps, w.eps):
+            zo.zo_perturb(t, k, e, 0, 0)
+    c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
+    zo.zo_update(t, c, w.lr, 0, 0)
+    want, co = oracle.full_step(th, "f32", 0, 0, 0, w.eps, w.lr, lp, lm, l0)
+    np.testing.assert_array_equal(c, co["c"])
+    assert_f32_update_close(t.cpu().numpy(), want, c, w.lr)
+
+
+# ----------------------------------------------------------------------------- full size
+def _windows(n, rng, count=24, size=1 << 15, boundaries=()):
+    starts = [0, n - size, n - 37] + [int(b) - size // 2 for b in boundaries]
+    starts += [int(s) for s in rng.integers(0, n - size, count)]
+    return sorted({min(max(s, 0), n - 1) for s in starts})
+
+
+@pytest.mark.parametrize("name,K", [("opt125m", 16), ("opt13b", 16), ("opt1.3b", 64), ("opt30b", 32)])
+def test_full_size_sampled_windows(name, K):
+    """At the full OPT-shaped size, in the benchmark's launch configuration: one perturb and one
+    update checked on windows (first, last incl. the ragged tail, tensor boundaries, random)."""
+    w = workloads.WORKLOADS[name]
+    n = w.n
+    note(f"full-size {name}: n {n} K {K}")
+    buf = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    workloads.fill_opt_buffer_device(buf, w)
+    rng = np.random.default_rng(7)
+    offs = [o for _, o, _ in workloads.tensor_offsets(w)]
+    bounds = [offs[1], offs[2], offs[len(offs) // 2], offs[-2]]
+    size = 1 << 15
+    wins = _windows(n, rng, 24, size, bounds)
+    grab = lambda: [host_bits(buf[s:min(s + size, n)]) for s in wins]
+    seed, step = 2024, 3
+    before = grab()
+    zo.zo_perturb(buf, 5, w.eps, seed, step)
+    mid = grab()
+    lp, lm, l0 = workloads.synthetic_losses(K, step)
+    c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
+    zo.zo_update(buf, c, w.lr, seed, step)
+    after = grab()
+    torch.cuda.synchronize()
+    del buf
+    torch.cuda.empty_cache()
+    for s, b, m, a in zip(wins, before, mid, after):
+        np.testing.assert_array_equal(m, oracle.perturb(b, "bf16", s, seed, step, 5, w.eps))
+        assert_bf16_within_1ulp(a, oracle.update(m, "bf16", s, seed, step, c, w.lr), m, c, w.lr)
