@@ -3,16 +3,25 @@
 // zo_perturb applies theta + eps z_k (Algorithm 1's +eps / -2 eps / +eps applications),
 // zo_update applies theta - lr sum_k c_k z_k in one pass (section 4.2, Eq. 6), and
 // zo_gen_bits exposes the probe generator. Probes are regenerated in registers from
-// (seed, step, k, element index) with Philox4x32-10 (Salmon et al., SC'11), one block per
-// 16-element tile and probe group of 8, 8 probe signs per byte (section 4.3); nothing but
-// theta touches HBM.
+// (seed, step, k, element index) with Philox4x32-10 (Salmon et al., SC'11): one 128-bit
+// block per 16-element tile and probe group of 8, 8 probe signs per byte (section 4.3).
+// Nothing but theta touches HBM.
 //
-// Work decomposition: a persistent grid-stride loop over tiles. A lane owns one tile per
-// iteration: 16 elements, i.e. 32 bytes of bf16 or 64 bytes of fp32 moved with 16-byte
-// non-temporal loads and stores (theta is streamed once per sweep; nothing is reused).
-// The update keeps, per probe group, a 256-entry table in LDS: entry b is the signed sum
-// of the group's 8 coefficients selected by the bits of b, so applying 8 probes to an
-// element costs one byte extract and one LDS read instead of 8 sign selects.
+// Memory layout of a sweep. theta is streamed in chunks of 64 x kU contiguous 16-byte
+// vectors per wave: vector u of lane l is chunk vector 64u + l, so every load and store
+// instruction of a wave covers 1 KiB of contiguous memory (non-temporal: nothing is
+// reused). A tile therefore spans kLanesPerTile adjacent lanes (2 for bf16, 4 for fp32).
+// Those lanes split the tile blocks of the chunk between them (each lane runs Philox for
+// kU / kLanesPerTile tiles) and hand each other the 32-bit words they need with DPP lane
+// swaps: bf16 lane pairs swap two words per block pair, fp32 lane quads transpose a 4x4
+// word matrix in two butterfly stages. Head and tail elements that do not fill a chunk
+// (and everything, when the storage is not 16-byte aligned relative to the global index)
+// take an element-wise path, one tile per lane.
+//
+// The update keeps, per probe group, a 256-entry table in LDS: entry b is the signed sum of
+// the group's 8 coefficients selected by the bits of b (pairwise). Applying 8 probes to an
+// element costs a byte extract and an LDS read. Groups accumulate in fp32, sequentially
+// within runs of 8 groups and with Neumaier compensation across runs.
 //
 // Built with -ffp-contract=off: every product and sum is rounded as written.
 
@@ -25,17 +34,18 @@
 
 namespace {
 
-constexpr uint32_t kTile = 16;       // elements per generator block
-constexpr uint32_t kBlock = 256;     // threads per workgroup
-constexpr uint32_t kDefaultMaxBlocks = 8192;
+constexpr uint32_t kTile = 16;    // elements per generator block
+constexpr uint32_t kBlock = 256;  // threads per workgroup (4 waves)
+constexpr uint32_t kWavesPerBlock = kBlock / 64;
+constexpr int kU = 4;             // 16-byte vectors per lane per chunk
+constexpr uint32_t kDefaultMaxBlocks = 65536;
 constexpr int kRounds = 10;
 
 uint32_t g_max_blocks = 0;  // 0: default
 
 // ---------------------------------------------------------------------------------------
 // Philox4x32-R: round (x0,x1,x2,x3) -> (hi(M1 x2)^x1^k0, lo(M1 x2), hi(M0 x0)^x3^k1, lo(M0 x0)),
-// key bumped by the Weyl constants after each round. The 32x32->64 products map to
-// v_mad_u64_u32.
+// key bumped by the Weyl constants after each round. 32x32->64 products: v_mad_u64_u32.
 __device__ __forceinline__ uint4 philox4x32(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
                                             uint32_t k0, uint32_t k1) {
 #pragma unroll
@@ -54,18 +64,26 @@ __device__ __forceinline__ uint4 philox4x32(uint32_t x0, uint32_t x1, uint32_t x
   return make_uint4(x0, x1, x2, x3);
 }
 
-__device__ __forceinline__ uint4 tile_block(uint64_t t, uint32_t step, uint32_t group, uint32_t k0,
-                                            uint32_t k1) {
-  return philox4x32(static_cast<uint32_t>(t), static_cast<uint32_t>(t >> 32), step, group, k0, k1);
-}
+struct Gen {
+  uint32_t k0, k1, step;
+  __device__ __forceinline__ uint4 block(uint64_t t, uint32_t group) const {
+    return philox4x32(static_cast<uint32_t>(t), static_cast<uint32_t>(t >> 32), step, group, k0, k1);
+  }
+};
 
-// Byte j (0..15) of a tile's block: byte (j mod 4) of word j / 4.
-__device__ __forceinline__ uint32_t block_byte(const uint32_t (&x)[4], int j) {
-  return (x[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+// Byte e (0..3) of a generator word: the probe byte of one element.
+__device__ __forceinline__ uint32_t word_byte(uint32_t w, int e) { return (w >> (8 * e)) & 0xFFu; }
+
+// Lane exchanges inside a quad (DPP quad_perm): swap with lane ^ 1, with lane ^ 2.
+__device__ __forceinline__ uint32_t swap_lane1(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ uint32_t swap_lane2(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x4E, 0xF, 0xF, false));
 }
 
 // ---------------------------------------------------------------------------------------
-// Storage formats. A tile is moved as 16-byte vectors; values are widened to fp32.
+// Storage formats.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -80,33 +98,23 @@ __device__ __forceinline__ void st_stream(void* p, u32x4 v) {
 // fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const f32x2 v = {lo, hi};
-  const bf16x2 r = __builtin_convertvector(v, bf16x2);
-  return __builtin_bit_cast(uint32_t, r);
-}
-__device__ __forceinline__ uint16_t to_bf16(float v) {
-  return static_cast<uint16_t>(pack_bf16x2(v, 0.0f) & 0xFFFFu);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
+// A storage type moves 16-byte vectors of kVecElems elements, widened to fp32. kLanesPerTile
+// adjacent lanes hold one 16-element tile; each of them needs kWords of the tile's 4
+// generator words (word w carries the probe bytes of tile elements 4w .. 4w+3).
 struct F32 {
   typedef float storage;
-  static constexpr uint32_t bytes = 4;
-  __device__ static __forceinline__ void load_tile(const storage* p, float (&v)[kTile]) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const u32x4 w = ld_stream(p + 4 * q);
-      v[4 * q + 0] = __uint_as_float(w.x);
-      v[4 * q + 1] = __uint_as_float(w.y);
-      v[4 * q + 2] = __uint_as_float(w.z);
-      v[4 * q + 3] = __uint_as_float(w.w);
-    }
+  static constexpr int kVecElems = 4, kLanesPerTile = 4, kWords = 1;
+  __device__ static __forceinline__ void unpack(u32x4 d, float (&v)[kVecElems]) {
+    v[0] = __uint_as_float(d.x);
+    v[1] = __uint_as_float(d.y);
+    v[2] = __uint_as_float(d.z);
+    v[3] = __uint_as_float(d.w);
   }
-  __device__ static __forceinline__ void store_tile(storage* p, const float (&v)[kTile]) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const u32x4 w = {__float_as_uint(v[4 * q]), __float_as_uint(v[4 * q + 1]),
-                       __float_as_uint(v[4 * q + 2]), __float_as_uint(v[4 * q + 3])};
-      st_stream(p + 4 * q, w);
-    }
+  __device__ static __forceinline__ u32x4 pack(const float (&v)[kVecElems]) {
+    return u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
   }
   __device__ static __forceinline__ float load1(const storage* p) { return *p; }
   __device__ static __forceinline__ void store1(storage* p, float v) { *p = v; }
@@ -114,78 +122,146 @@ struct F32 {
 
 struct BF16 {
   typedef uint16_t storage;
-  static constexpr uint32_t bytes = 2;
-  __device__ static __forceinline__ void load_tile(const storage* p, float (&v)[kTile]) {
+  static constexpr int kVecElems = 8, kLanesPerTile = 2, kWords = 2;
+  __device__ static __forceinline__ void unpack(u32x4 d, float (&v)[kVecElems]) {
+    const uint32_t w[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const u32x4 w = ld_stream(p + 8 * q);
-      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        v[8 * q + 2 * m] = __uint_as_float(ws[m] << 16);
-        v[8 * q + 2 * m + 1] = __uint_as_float(ws[m] & 0xFFFF0000u);
-      }
+    for (int m = 0; m < 4; ++m) {
+      v[2 * m] = __uint_as_float(w[m] << 16);
+      v[2 * m + 1] = __uint_as_float(w[m] & 0xFFFF0000u);
     }
   }
-  __device__ static __forceinline__ void store_tile(storage* p, const float (&v)[kTile]) {
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const u32x4 w = {pack_bf16x2(v[8 * q + 0], v[8 * q + 1]), pack_bf16x2(v[8 * q + 2], v[8 * q + 3]),
-                       pack_bf16x2(v[8 * q + 4], v[8 * q + 5]), pack_bf16x2(v[8 * q + 6], v[8 * q + 7])};
-      st_stream(p + 8 * q, w);
-    }
+  __device__ static __forceinline__ u32x4 pack(const float (&v)[kVecElems]) {
+    return u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                 pack_bf16x2(v[6], v[7])};
   }
   __device__ static __forceinline__ float load1(const storage* p) {
     return __uint_as_float(static_cast<uint32_t>(*p) << 16);
   }
-  __device__ static __forceinline__ void store1(storage* p, float v) { *p = to_bf16(v); }
+  __device__ static __forceinline__ void store1(storage* p, float v) {
+    *p = static_cast<uint16_t>(pack_bf16x2(v, 0.0f) & 0xFFFFu);
+  }
 };
 
-// Range of global elements [lo, hi) covered by a launch and the tiles that touch it.
-struct Span {
-  uint64_t lo, hi;       // global element indices
-  uint64_t t_first;      // first tile
-  uint64_t n_tiles;      // tiles touching [lo, hi)
+template <class S>
+struct ChunkShape {
+  static constexpr uint64_t kVecs = 64ull * kU;                      // vectors per chunk
+  static constexpr uint64_t kElems = kVecs * S::kVecElems;           // bf16 2048, fp32 1024
+  static constexpr uint64_t kTiles = kElems / kTile;                 // bf16 128, fp32 64
+  static constexpr int kOwn = kU / S::kLanesPerTile;                 // blocks a lane generates
 };
 
-// Apply f(j, value) -> value to the elements of tile t inside the span. VEC: the tile's
-// storage is 16-byte aligned, so full tiles move as vectors; edge tiles go element-wise.
-template <class S, bool VEC, class F>
-__device__ __forceinline__ void apply_tile(typename S::storage* params, const Span& sp, uint64_t t, F f) {
+// For chunk vector base vbase (a global vector index, multiple of 64 kU) and probe group g:
+// W[u][w] = the generator words this lane's vector u needs. Lanes 2m, 2m+1 (bf16) or
+// 4m .. 4m+3 (fp32) share the tiles T(u) = (vbase + 64u) / kLanesPerTile + m.
+__device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
+                                            uint32_t (&W)[kU][BF16::kWords], BF16) {
+  const uint32_t q = lane & 1u;
+  const uint64_t t0 = vbase / 2 + (lane >> 1);
+#pragma unroll
+  for (int j = 0; j < kU / 2; ++j) {
+    // this lane generates tile u = 2j + q; it needs words 2q, 2q+1 of tiles 2j and 2j+1
+    const uint4 r = gen.block(t0 + 32ull * (2 * j + q), group);
+    const uint32_t own0 = q ? r.z : r.x, own1 = q ? r.w : r.y;
+    const uint32_t got0 = swap_lane1(q ? r.x : r.z), got1 = swap_lane1(q ? r.y : r.w);
+    W[2 * j][0] = q ? got0 : own0;
+    W[2 * j][1] = q ? got1 : own1;
+    W[2 * j + 1][0] = q ? own0 : got0;
+    W[2 * j + 1][1] = q ? own1 : got1;
+  }
+}
+
+__device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
+                                            uint32_t (&W)[kU][F32::kWords], F32) {
+  // lane q of the quad generates tile T(q); after a 4x4 transpose across the quad, register
+  // u of lane q holds word q of tile T(u).
+  const uint32_t q = lane & 3u;
+  const uint4 r = gen.block(vbase / 4 + 16ull * q + (lane >> 2), group);
+  uint32_t a[4] = {r.x, r.y, r.z, r.w};
+  const bool hi1 = q & 1u, hi2 = q & 2u;
+#pragma unroll
+  for (int r0 = 0; r0 < 4; r0 += 2) {  // exchange off-diagonal elements of each 2x2 block
+    const uint32_t got = swap_lane1(hi1 ? a[r0] : a[r0 + 1]);
+    if (hi1) a[r0] = got; else a[r0 + 1] = got;
+  }
+#pragma unroll
+  for (int r0 = 0; r0 < 2; ++r0) {     // exchange off-diagonal 2x2 blocks
+    const uint32_t got = swap_lane2(hi2 ? a[r0] : a[r0 + 2]);
+    if (hi2) a[r0] = got; else a[r0 + 2] = got;
+  }
+#pragma unroll
+  for (int u = 0; u < kU; ++u) W[u][0] = a[u];
+}
+
+// Probe byte of element e (0 .. kVecElems-1) of a vector, from its words.
+template <class S>
+__device__ __forceinline__ uint32_t elem_byte(const uint32_t (&w)[S::kWords], int e) {
+  return word_byte(w[e >> 2], e & 3);
+}
+
+// Element-wise path: elements of tile t inside [lo, hi), one lane.
+template <class S, class F>
+__device__ __forceinline__ void tile_elementwise(typename S::storage* params, uint64_t lo, uint64_t hi, uint64_t t,
+                                                 F f) {
   const uint64_t g0 = t * kTile;
-  if (VEC && g0 >= sp.lo && g0 + kTile <= sp.hi) {
-    typename S::storage* p = params + (g0 - sp.lo);
-    float v[kTile];
-    S::load_tile(p, v);
 #pragma unroll
-    for (int j = 0; j < (int)kTile; ++j) v[j] = f(j, v[j]);
-    S::store_tile(p, v);
-  } else {
-#pragma unroll
-    for (int j = 0; j < (int)kTile; ++j) {
-      const uint64_t g = g0 + j;
-      if (g >= sp.lo && g < sp.hi) {
-        typename S::storage* p = params + (g - sp.lo);
-        S::store1(p, f(j, S::load1(p)));
-      }
+  for (int j = 0; j < (int)kTile; ++j) {
+    const uint64_t g = g0 + j;
+    if (g >= lo && g < hi) {
+      typename S::storage* p = params + (g - lo);
+      S::store1(p, f(j, S::load1(p)));
     }
   }
 }
 
+// What a launch covers: global elements [lo, hi); full chunks [c_first, c_first + n_chunks)
+// take the vector path; the remaining edge tiles are [head_t0, +head_nt) and [tail_t0, +tail_nt).
+struct Plan {
+  uint64_t lo, hi;
+  uint64_t c_first, n_chunks;
+  uint64_t head_t0, head_nt, tail_t0, tail_nt;
+};
+
+__device__ __forceinline__ uint64_t edge_tile(const Plan& pl, uint64_t j) {
+  return j < pl.head_nt ? pl.head_t0 + j : pl.tail_t0 + (j - pl.head_nt);
+}
+
 // ---------------------------------------------------------------------------------------
-// perturb: theta + eps * z_k. One generator block per tile; bit (k mod 8) of each byte.
-template <class S, bool VEC>
-__global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* params, Span sp, uint32_t k0,
-                                                        uint32_t k1, uint32_t step, uint32_t group,
-                                                        uint32_t bit, float eps) {
+// perturb: theta + eps * z_k (bit k mod 8 of each probe byte of group k / 8).
+template <class S>
+__global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* params, Plan pl, Gen gen,
+                                                        uint32_t group, uint32_t bit, float eps) {
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
+  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
+       c += n_waves) {
+    const uint64_t vbase = (pl.c_first + c) * ChunkShape<S>::kVecs;
+    char* base = reinterpret_cast<char*>(params) +
+                 (vbase * S::kVecElems - pl.lo) * sizeof(typename S::storage);
+    u32x4 d[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
+    uint32_t W[kU][S::kWords];
+    chunk_words(gen, vbase, lane, group, W, S());
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      float v[S::kVecElems];
+      S::unpack(d[u], v);
+#pragma unroll
+      for (int e = 0; e < S::kVecElems; ++e) v[e] += ((elem_byte<S>(W[u], e) >> bit) & 1u) ? eps : -eps;
+      d[u] = S::pack(v);
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
+  }
+  const uint64_t n_edge = pl.head_nt + pl.tail_nt;
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; i < sp.n_tiles; i += stride) {
-    const uint64_t t = sp.t_first + i;
-    const uint4 r = tile_block(t, step, group, k0, k1);
+  for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
+    const uint64_t t = edge_tile(pl, j);
+    const uint4 r = gen.block(t, group);
     const uint32_t x[4] = {r.x, r.y, r.z, r.w};
-    apply_tile<S, VEC>(params, sp, t, [&](int j, float v) {
-      const bool plus = (block_byte(x, j) >> bit) & 1u;
-      return v + (plus ? eps : -eps);
+    tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) {
+      return v + (((word_byte(x[e >> 2], e & 3) >> bit) & 1u) ? eps : -eps);
     });
   }
 }
@@ -196,44 +272,11 @@ struct Coefs {
   float c[ZO_K_MAX];
 };
 
-// Sum of the table values of groups [LO, HI) of the launch for the 16 elements of a tile,
-// pairwise (a balanced tree over groups). Groups at or past n_groups contribute 0.
-template <int LO, int HI, bool GUARD>
-__device__ __forceinline__ void group_tree(float (&out)[kTile], const float* tab, uint64_t t, uint32_t step,
-                                           uint32_t g_first, uint32_t g_chunk, uint32_t n_groups,
-                                           uint32_t k0, uint32_t k1) {
-  if constexpr (HI - LO == 1) {
-    const uint32_t g = g_chunk + LO;
-    if (GUARD && g >= n_groups) {
-#pragma unroll
-      for (int j = 0; j < (int)kTile; ++j) out[j] = 0.0f;
-      return;
-    }
-    const uint4 r = tile_block(t, step, g_first + g, k0, k1);
-    const uint32_t x[4] = {r.x, r.y, r.z, r.w};
-    const float* tg = tab + 256u * g;
-#pragma unroll
-    for (int j = 0; j < (int)kTile; ++j) out[j] = tg[block_byte(x, j)];
-  } else {
-    constexpr int MID = (LO + HI) / 2;
-    float a[kTile], b[kTile];
-    group_tree<LO, MID, GUARD>(a, tab, t, step, g_first, g_chunk, n_groups, k0, k1);
-    group_tree<MID, HI, GUARD>(b, tab, t, step, g_first, g_chunk, n_groups, k0, k1);
-#pragma unroll
-    for (int j = 0; j < (int)kTile; ++j) out[j] = a[j] + b[j];
-  }
-}
-
-// NG > 0: exactly NG groups (compile time), pairwise over groups.
-// NG == 0: any number of groups; chunks of 8 groups summed pairwise, chunks compensated.
-template <class S, bool VEC, int NG>
-__global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* params, Span sp, uint32_t k0,
-                                                       uint32_t k1, uint32_t step, uint32_t k_base,
-                                                       uint32_t K, uint32_t n_groups, Coefs cf, float lr) {
-  extern __shared__ float tab[];  // n_groups x 256
+// Build the n_groups x 256 table in LDS. Entry (g, b): sum over the group's 8 probe slots
+// of +-c (bit set: +c); slots outside [k_base, k_base + K) contribute 0; pairwise.
+__device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
+                                             uint32_t n_groups) {
   const uint32_t g_first = k_base / 8;
-  // Table entry (g, b): sum over the group's 8 probe slots of +-c (bit set: +c), slots
-  // outside [k_base, k_base + K) contributing 0; summed pairwise.
   for (uint32_t e = threadIdx.x; e < n_groups * 256u; e += kBlock) {
     const uint32_t g = e >> 8, b = e & 255u;
     float v[8];
@@ -247,53 +290,154 @@ __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* par
     tab[e] = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
   }
   __syncthreads();
+}
 
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; i < sp.n_tiles; i += stride) {
-    const uint64_t t = sp.t_first + i;
-    float acc[kTile];
-    if constexpr (NG > 0) {
-      group_tree<0, NG, false>(acc, tab, t, step, g_first, 0, NG, k0, k1);
-    } else {
-      float comp[kTile];
+// acc[u][e] (+)= table value of group g for each element of the chunk.
+template <class S, bool FIRST>
+__device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
+                                          uint64_t vbase, uint32_t lane, uint32_t g, uint32_t g_first) {
+  uint32_t W[kU][S::kWords];
+  chunk_words(gen, vbase, lane, g_first + g, W, S());
+  const float* tg = tab + 256u * g;
 #pragma unroll
-      for (int j = 0; j < (int)kTile; ++j) acc[j] = comp[j] = 0.0f;
-      for (uint32_t gc = 0; gc < n_groups; gc += 8) {
-        float part[kTile];
-        group_tree<0, 8, true>(part, tab, t, step, g_first, gc, n_groups, k0, k1);
-        // Kahan-Babuska (Neumaier) compensated accumulation across chunks.
+  for (int u = 0; u < kU; ++u)
 #pragma unroll
-        for (int j = 0; j < (int)kTile; ++j) {
-          const float s = acc[j] + part[j];
-          comp[j] += (fabsf(acc[j]) >= fabsf(part[j])) ? ((acc[j] - s) + part[j]) : ((part[j] - s) + acc[j]);
-          acc[j] = s;
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < (int)kTile; ++j) acc[j] = acc[j] + comp[j];
+    for (int e = 0; e < S::kVecElems; ++e) {
+      const float x = tg[elem_byte<S>(W[u], e)];
+      acc[u][e] = FIRST ? x : acc[u][e] + x;
     }
-    apply_tile<S, VEC>(params, sp, t, [&](int j, float v) { return v - lr * acc[j]; });
+}
+
+// Sum of the tables of groups 0 .. n_groups-1 for the chunk: NG > 0 fixes the count at
+// compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
+template <class S, int NG>
+__device__ __forceinline__ void chunk_sums(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
+                                           uint64_t vbase, uint32_t lane, uint32_t n_groups, uint32_t g_first) {
+  if constexpr (NG > 0) {
+    add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first);
+#pragma unroll
+    for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first);
+  } else {
+    float comp[kU][S::kVecElems];
+    for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
+      float part[kU][S::kVecElems];
+      add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first);
+      const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
+      for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first);
+#pragma unroll
+      for (int u = 0; u < kU; ++u)
+#pragma unroll
+        for (int e = 0; e < S::kVecElems; ++e) {
+          if (g0 == 0) {
+            acc[u][e] = part[u][e];
+            comp[u][e] = 0.0f;
+          } else {
+            const float a = acc[u][e], p = part[u][e], s = a + p;
+            comp[u][e] += fabsf(a) >= fabsf(p) ? (a - s) + p : (p - s) + a;
+            acc[u][e] = s;
+          }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int e = 0; e < S::kVecElems; ++e) acc[u][e] = acc[u][e] + comp[u][e];
+  }
+}
+
+// Same sum for one tile on the element-wise path (one lane, all 16 elements).
+__device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab, const Gen& gen, uint64_t t,
+                                          uint32_t n_groups, uint32_t g_first) {
+  float comp[kTile];
+  for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
+    float part[kTile];
+    const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
+    for (uint32_t g = g0; g < g1; ++g) {
+      const uint4 r = gen.block(t, g_first + g);
+      const uint32_t x[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+      for (int j = 0; j < (int)kTile; ++j) {
+        const float v = tab[256u * g + word_byte(x[j >> 2], j & 3)];
+        part[j] = g == g0 ? v : part[j] + v;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < (int)kTile; ++j) {
+      if (g0 == 0) {
+        acc[j] = part[j];
+        comp[j] = 0.0f;
+      } else {
+        const float a = acc[j], p = part[j], s = a + p;
+        comp[j] += fabsf(a) >= fabsf(p) ? (a - s) + p : (p - s) + a;
+        acc[j] = s;
+      }
+    }
+  }
+  if (n_groups > 8) {
+#pragma unroll
+    for (int j = 0; j < (int)kTile; ++j) acc[j] = acc[j] + comp[j];
+  }
+}
+
+template <class S, int NG>
+__global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* params, Plan pl, Gen gen,
+                                                       uint32_t k_base, uint32_t K, uint32_t n_groups, Coefs cf,
+                                                       float lr) {
+  extern __shared__ float tab[];  // n_groups x 256
+  build_tables(tab, cf, k_base, K, n_groups);
+  const uint32_t g_first = k_base / 8;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
+  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
+       c += n_waves) {
+    const uint64_t vbase = (pl.c_first + c) * ChunkShape<S>::kVecs;
+    char* base = reinterpret_cast<char*>(params) +
+                 (vbase * S::kVecElems - pl.lo) * sizeof(typename S::storage);
+    u32x4 d[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
+    float acc[kU][S::kVecElems];
+    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      float v[S::kVecElems];
+      S::unpack(d[u], v);
+#pragma unroll
+      for (int e = 0; e < S::kVecElems; ++e) v[e] = v[e] - lr * acc[u][e];
+      d[u] = S::pack(v);
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
+  }
+  const uint64_t n_edge = pl.head_nt + pl.tail_nt;
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
+  for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
+    const uint64_t t = edge_tile(pl, j);
+    float acc[kTile];
+    tile_sums(acc, tab, gen, t, n_groups, g_first);
+    tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) { return v - lr * acc[e]; });
   }
 }
 
 // ---------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void gen_bits_kernel(uint8_t* out, uint64_t tile_begin, uint64_t n_tiles,
-                                                         uint32_t step, uint32_t group, uint32_t k0,
-                                                         uint32_t k1) {
+                                                         uint32_t group, Gen gen) {
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
   for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n_tiles; i += stride) {
-    const uint4 r = tile_block(tile_begin + i, step, group, k0, k1);
-    const u32x4 w = {r.x, r.y, r.z, r.w};
-    *reinterpret_cast<u32x4*>(out + 16 * i) = w;
+    const uint4 r = gen.block(tile_begin + i, group);
+    *reinterpret_cast<u32x4*>(out + 16 * i) = u32x4{r.x, r.y, r.z, r.w};
   }
 }
 
 // ---------------------------------------------------------------------------------------
 // Host side.
-uint32_t grid_for(uint64_t n_tiles) {
-  const uint64_t cap = g_max_blocks ? g_max_blocks : kDefaultMaxBlocks;
-  const uint64_t need = (n_tiles + kBlock - 1) / kBlock;
-  return static_cast<uint32_t>(need < cap ? need : cap);
+uint32_t cap_blocks() { return g_max_blocks ? g_max_blocks : kDefaultMaxBlocks; }
+
+uint32_t grid_for(uint64_t work_items, uint64_t per_block) {
+  const uint64_t need = (work_items + per_block - 1) / per_block;
+  const uint64_t cap = cap_blocks();
+  const uint64_t g = need < cap ? need : cap;
+  return static_cast<uint32_t>(g ? g : 1);
 }
 
 int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n, size_t* elem) {
@@ -302,48 +446,74 @@ int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n, s
   if (n == 0) return ZO_OK;
   if (params == nullptr) return ZO_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(params) % *elem != 0) return ZO_ERR_ARG;
-  if (offset + n < offset) return ZO_ERR_ARG;  // wraps past 2^64
+  if (offset + n < offset || offset + n == 0) return ZO_ERR_ARG;  // reaches 2^64
   return ZO_OK;
 }
 
-Span make_span(uint64_t offset, uint64_t n) {
-  Span sp;
-  sp.lo = offset;
-  sp.hi = offset + n;
-  sp.t_first = offset / kTile;
-  sp.n_tiles = (sp.hi - 1) / kTile - sp.t_first + 1;
-  return sp;
+uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
+
+// Full chunks need the address of global element 0 (params shifted back by offset
+// elements) to be 16-byte aligned, so that every chunk vector is an aligned 16 bytes.
+Plan make_plan(const void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t chunk_elems) {
+  Plan pl{};
+  pl.lo = offset;
+  pl.hi = offset + n;
+  const uintptr_t base = reinterpret_cast<uintptr_t>(params) - static_cast<uintptr_t>(offset * elem);
+  uint64_t head_end = pl.hi, tail_begin = pl.hi;
+  if ((base & 15u) == 0) {
+    const uint64_t c0 = ceil_div(pl.lo, chunk_elems), c1 = pl.hi / chunk_elems;
+    if (c0 < c1) {
+      pl.c_first = c0;
+      pl.n_chunks = c1 - c0;
+      head_end = c0 * chunk_elems;
+      tail_begin = c1 * chunk_elems;
+    }
+  }
+  if (head_end > pl.lo) {
+    pl.head_t0 = pl.lo / kTile;
+    pl.head_nt = ceil_div(head_end, kTile) - pl.head_t0;
+  }
+  if (pl.hi > tail_begin) {
+    pl.tail_t0 = tail_begin / kTile;
+    pl.tail_nt = ceil_div(pl.hi, kTile) - pl.tail_t0;
+  }
+  return pl;
 }
 
-// Full tiles can move as 16-byte vectors iff the address of global element 0 (params
-// shifted back by offset elements) is 16-byte aligned, since tiles span 32 or 64 bytes.
-bool vector_ok(const void* params, uint64_t offset, size_t elem) {
-  const uintptr_t base = reinterpret_cast<uintptr_t>(params) - static_cast<uintptr_t>(offset * elem);
-  return (base & 15u) == 0;
+uint32_t plan_grid(const Plan& pl) {
+  const uint32_t a = pl.n_chunks ? grid_for(pl.n_chunks, kWavesPerBlock) : 1;
+  const uint32_t b = grid_for(pl.head_nt + pl.tail_nt, kBlock);
+  return a > b ? a : b;
 }
 
 int launch_status() { return hipGetLastError() == hipSuccess ? ZO_OK : ZO_ERR_HIP; }
 
-template <class S, bool VEC>
-void launch_update(void* params, const Span& sp, uint32_t k0, uint32_t k1, uint32_t step, uint32_t k_base,
-                   uint32_t K, uint32_t n_groups, const Coefs& cf, float lr, hipStream_t st) {
-  const dim3 grid(grid_for(sp.n_tiles)), block(kBlock);
+template <class S>
+void launch_perturb(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k, float eps,
+                    hipStream_t st) {
+  const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
+  perturb_kernel<S><<<dim3(plan_grid(pl)), dim3(kBlock), 0, st>>>(static_cast<typename S::storage*>(params), pl,
+                                                                   gen, k / 8, k % 8, eps);
+}
+
+template <class S>
+void launch_update(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k_base, uint32_t K,
+                   uint32_t n_groups, const Coefs& cf, float lr, hipStream_t st) {
+  const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
+  const dim3 grid(plan_grid(pl)), block(kBlock);
   const size_t lds = static_cast<size_t>(n_groups) * 256 * sizeof(float);
   auto* p = static_cast<typename S::storage*>(params);
   switch (n_groups) {
-    case 1: update_kernel<S, VEC, 1><<<grid, block, lds, st>>>(p, sp, k0, k1, step, k_base, K, n_groups, cf, lr); break;
-    case 2: update_kernel<S, VEC, 2><<<grid, block, lds, st>>>(p, sp, k0, k1, step, k_base, K, n_groups, cf, lr); break;
-    case 4: update_kernel<S, VEC, 4><<<grid, block, lds, st>>>(p, sp, k0, k1, step, k_base, K, n_groups, cf, lr); break;
-    case 8: update_kernel<S, VEC, 8><<<grid, block, lds, st>>>(p, sp, k0, k1, step, k_base, K, n_groups, cf, lr); break;
-    default: update_kernel<S, VEC, 0><<<grid, block, lds, st>>>(p, sp, k0, k1, step, k_base, K, n_groups, cf, lr); break;
+    case 1: update_kernel<S, 1><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
+    case 2: update_kernel<S, 2><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
+    case 4: update_kernel<S, 4><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
+    case 8: update_kernel<S, 8><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
+    default: update_kernel<S, 0><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
   }
 }
 
-template <class S, bool VEC>
-void launch_perturb(void* params, const Span& sp, uint32_t k0, uint32_t k1, uint32_t step, uint32_t k,
-                    float eps, hipStream_t st) {
-  perturb_kernel<S, VEC><<<dim3(grid_for(sp.n_tiles)), dim3(kBlock), 0, st>>>(
-      static_cast<typename S::storage*>(params), sp, k0, k1, step, k / 8, k % 8, eps);
+Gen make_gen(uint64_t seed, uint32_t step) {
+  return Gen{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), step};
 }
 
 }  // namespace
@@ -357,18 +527,13 @@ int zo_perturb(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64
   if (rc != ZO_OK) return rc;
   if (!std::isfinite(eps)) return ZO_ERR_NONFINITE;
   if (n == 0) return ZO_OK;
-  const Span sp = make_span(offset, n);
-  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
+  const Gen gen = make_gen(seed, step);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const bool vec = vector_ok(params, offset, elem);
   (void)hipGetLastError();
-  if (dtype == ZO_F32) {
-    vec ? launch_perturb<F32, true>(params, sp, k0, k1, step, k, eps, st)
-        : launch_perturb<F32, false>(params, sp, k0, k1, step, k, eps, st);
-  } else {
-    vec ? launch_perturb<BF16, true>(params, sp, k0, k1, step, k, eps, st)
-        : launch_perturb<BF16, false>(params, sp, k0, k1, step, k, eps, st);
-  }
+  if (dtype == ZO_F32)
+    launch_perturb<F32>(params, offset, n, gen, k, eps, st);
+  else
+    launch_perturb<BF16>(params, offset, n, gen, k, eps, st);
   return launch_status();
 }
 
@@ -389,18 +554,13 @@ int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint
   const uint32_t g_first = k_base / 8;
   const uint32_t g_last = static_cast<uint32_t>((static_cast<uint64_t>(k_base) + K - 1) / 8);
   const uint32_t n_groups = g_last - g_first + 1;
-  const Span sp = make_span(offset, n);
-  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
+  const Gen gen = make_gen(seed, step);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const bool vec = vector_ok(params, offset, elem);
   (void)hipGetLastError();
-  if (dtype == ZO_F32) {
-    vec ? launch_update<F32, true>(params, sp, k0, k1, step, k_base, K, n_groups, cf, lr, st)
-        : launch_update<F32, false>(params, sp, k0, k1, step, k_base, K, n_groups, cf, lr, st);
-  } else {
-    vec ? launch_update<BF16, true>(params, sp, k0, k1, step, k_base, K, n_groups, cf, lr, st)
-        : launch_update<BF16, false>(params, sp, k0, k1, step, k_base, K, n_groups, cf, lr, st);
-  }
+  if (dtype == ZO_F32)
+    launch_update<F32>(params, offset, n, gen, k_base, K, n_groups, cf, lr, st);
+  else
+    launch_update<BF16>(params, offset, n, gen, k_base, K, n_groups, cf, lr, st);
   return launch_status();
 }
 
@@ -416,8 +576,8 @@ int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_
   if (reinterpret_cast<uintptr_t>(out_dev) % 16 != 0) return ZO_ERR_ARG;
   if (tile_begin >= (1ull << 60) || n_tiles > (1ull << 60) - tile_begin) return ZO_ERR_ARG;
   (void)hipGetLastError();
-  gen_bits_kernel<<<dim3(grid_for(n_tiles)), dim3(kBlock), 0, static_cast<hipStream_t>(stream)>>>(
-      out_dev, tile_begin, n_tiles, step, group, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
+  gen_bits_kernel<<<dim3(grid_for(n_tiles, kBlock)), dim3(kBlock), 0, static_cast<hipStream_t>(stream)>>>(
+      out_dev, tile_begin, n_tiles, group, make_gen(seed, step));
   return launch_status();
 }
 
