@@ -32,6 +32,23 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def measured_traffic(workload, K, dtype):
+    """HBM bytes per launch from the committed rocprofv3 counter summaries (FETCH_SIZE and
+    WRITE_SIZE, each scaled by a plain copy of known size), keyed by kernel; {} when no
+    summary matches this workload or the sweep source has changed since it was taken."""
+    import glob
+    import hashlib
+    src = os.path.join(ROOT, "paper_2609_38095_amd", "csrc", "zo_sweep.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*hbm_counters.md"))):
+        for line in open(path):
+            if line.startswith("traffic-json:"):
+                d = json.loads(line.split(":", 1)[1])
+                if (d.get("workload"), d.get("K"), d.get("dtype"), d.get("source_sha256")) == (workload, K, dtype, digest):
+                    return d["bytes_per_launch"]
+    return {}
+
+
 def cpu_baseline(w, K, budget_s=15.0):
     """The oracle on the host: one step (3K perturbs + one update) over a window of the workload."""
     import numpy as np
@@ -67,6 +84,8 @@ def main():
     ap.add_argument("--workload", default="opt13b", help="tiny, opt125m, opt1.3b, opt13b or opt30b")
     ap.add_argument("--K", type=int, default=0, help="probes per step (default: the workload's first)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-gib", type=float, default=0.0,
+                    help="before warmup, run one plain device copy of this many GiB (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -93,6 +112,16 @@ def main():
     else:
         theta.copy_(torch.from_numpy(workloads.tiny_theta(n)))
     torch.cuda.synchronize()
+    if args.calib_copy_gib > 0:
+        nb = int(args.calib_copy_gib * 2 ** 30)
+        src = torch.ones(nb, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {nb} bytes read, {nb} bytes written")
+        del src, dst
+        torch.cuda.empty_cache()
     stream = torch.cuda.current_stream(dev)
     seed = 2024
 
@@ -140,9 +169,13 @@ def main():
     p_ms, u_ms = float(ms["perturb"].mean()), float(ms["update"].mean())
     p_gbps, u_gbps = sweep_bytes / (p_ms * 1e-3) / 1e9, sweep_bytes / (u_ms * 1e-3) / 1e9
 
+    traffic = measured_traffic(w.name, K, w.dtype)
+
     def roof(kernel, avg_ms, gb):
+        d = ms["perturb" if kernel == "zo_perturb" else "update"]
         return {"kernel": kernel, "bound": "hbm", "achieved": round(gb, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(gb / HBM_PEAK_GBPS, 4), "traffic": None, "avg_ms": round(avg_ms, 4),
+                "frac": round(gb / HBM_PEAK_GBPS, 4), "traffic": traffic.get(kernel), "avg_ms": round(avg_ms, 4),
+                "min_ms": round(float(d.min()), 4), "max_ms": round(float(d.max()), 4), "launches": int(d.size),
                 "bytes_per_launch": sweep_bytes}
 
     out = {

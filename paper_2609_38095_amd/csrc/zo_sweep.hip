@@ -45,15 +45,21 @@ uint32_t g_max_blocks = 0;  // 0: default
 
 // ---------------------------------------------------------------------------------------
 // Philox4x32-R: round (x0,x1,x2,x3) -> (hi(M1 x2)^x1^k0, lo(M1 x2), hi(M0 x0)^x3^k1, lo(M0 x0)),
-// key bumped by the Weyl constants after each round. 32x32->64 products: v_mad_u64_u32.
+// key bumped by the Weyl constants after each round. 32x32->64 products: v_mad_u64_u32; each
+// three-way XOR is one v_bitop3_b32 (truth table 0x96), which the compiler does not form from
+// a ^ b ^ c by itself.
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 __device__ __forceinline__ uint4 philox4x32(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
                                             uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * x0;
     const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * x2;
-    const uint32_t y0 = static_cast<uint32_t>(p1 >> 32) ^ x1 ^ k0;
-    const uint32_t y2 = static_cast<uint32_t>(p0 >> 32) ^ x3 ^ k1;
+    const uint32_t y0 = xor3(static_cast<uint32_t>(p1 >> 32), x1, k0);
+    const uint32_t y2 = xor3(static_cast<uint32_t>(p0 >> 32), x3, k1);
     x1 = static_cast<uint32_t>(p1);
     x3 = static_cast<uint32_t>(p0);
     x0 = y0;
@@ -73,6 +79,12 @@ struct Gen {
 
 // Byte e (0..3) of a generator word: the probe byte of one element.
 __device__ __forceinline__ uint32_t word_byte(uint32_t w, int e) { return (w >> (8 * e)) & 0xFFu; }
+
+// Table entry selected by byte e of w, in a table of 256 floats (one SDWA shift for the address).
+__device__ __forceinline__ float table_at(const float* tab, uint32_t w, int e) {
+  const uint32_t off = ((w >> (8 * e)) & 0xFFu) << 2;
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + off);
+}
 
 // Lane exchanges inside a quad (DPP quad_perm): swap with lane ^ 1, with lane ^ 2.
 __device__ __forceinline__ uint32_t swap_lane1(uint32_t v) {
@@ -303,7 +315,7 @@ __device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const 
   for (int u = 0; u < kU; ++u)
 #pragma unroll
     for (int e = 0; e < S::kVecElems; ++e) {
-      const float x = tg[elem_byte<S>(W[u], e)];
+      const float x = table_at(tg, W[u][e >> 2], e & 3);
       acc[u][e] = FIRST ? x : acc[u][e] + x;
     }
 }
@@ -383,7 +395,10 @@ template <class S, int NG>
 __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* params, Plan pl, Gen gen,
                                                        uint32_t k_base, uint32_t K, uint32_t n_groups, Coefs cf,
                                                        float lr) {
-  extern __shared__ float tab[];  // n_groups x 256
+  // n_groups x 256 floats: static for a fixed group count (constant LDS offsets), else dynamic.
+  extern __shared__ float tab_dyn[];
+  __shared__ float tab_fix[NG > 0 ? NG * 256 : 1];
+  float* tab = NG > 0 ? tab_fix : tab_dyn;
   build_tables(tab, cf, k_base, K, n_groups);
   const uint32_t g_first = k_base / 8;
   const uint32_t lane = threadIdx.x & 63u;
@@ -501,7 +516,8 @@ void launch_update(void* params, uint64_t offset, uint64_t n, const Gen& gen, ui
                    uint32_t n_groups, const Coefs& cf, float lr, hipStream_t st) {
   const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
   const dim3 grid(plan_grid(pl)), block(kBlock);
-  const size_t lds = static_cast<size_t>(n_groups) * 256 * sizeof(float);
+  const bool fixed = n_groups == 1 || n_groups == 2 || n_groups == 4 || n_groups == 8;
+  const size_t lds = fixed ? 0 : static_cast<size_t>(n_groups) * 256 * sizeof(float);
   auto* p = static_cast<typename S::storage*>(params);
   switch (n_groups) {
     case 1: update_kernel<S, 1><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
