@@ -11,7 +11,8 @@ Modules:
   philox   -- Philox-4xW (Salmon et al., SC'11), generic in word width and rounds
   probes   -- Rademacher probes from (seed, step, k, element index), 8 probes per byte
   numerics -- bf16 storage format and single-step rounding
-  sweep    -- perturb (theta + e z_k) and the fused update (theta - lr sum_k c_k z_k)
+  sweep    -- perturb (theta + e z_k), the fused update (theta - lr sum_k c_k z_k), and the
+              fused transitions perturb2 / update_restore
   coeffs   -- curvature, alpha-saturated weight and per-probe coefficients
   step     -- one single-device step composed from the above
 
@@ -25,5 +26,5 @@ from .numerics import bf16_to_f32, bf16_to_f64, f32_to_bf16, f64_to_bf16, f64_to
 from .philox import philox4
 from .probes import (DEFAULT_ROUNDS, PROBES_PER_GROUP, TILE, element_bytes, materialize_Z,
                      signs, tile_bytes, tile_words)
-from .step import full_step
-from .sweep import perturb, perturb_schedule, probe_sum, update
+from .step import full_step, full_step_fused
+from .sweep import perturb, perturb2, perturb_schedule, probe_sum, update, update_restore

@@ -17,6 +17,13 @@ Arithmetic (readings; the paper does not fix it):
   * update: the sum over probes is accumulated in float64 from the float32 c_k, and
     theta - lr * sum is rounded once to the storage type.
 Weights are float32 numpy arrays, or uint16 arrays of bf16 bit patterns.
+
+Fused transitions (reading; the paper applies them as separate passes): on one device the
+restore of probe k (+eps) and the +eps of probe k+1 are consecutive applications, and so are
+the last restore and the update. perturb2 and update_restore apply such a pair in one pass:
+  perturb2       -- d = fl32(e_a z_a + e_b z_b) (exact when |e_a| = |e_b|), theta + d in one
+                    fp32 addition, then bf16 storage rounds to nearest-even;
+  update_restore -- theta + e_r z_r - lr * sum_k c_k z_k formed in float64 and rounded once.
 """
 
 import numpy as np
@@ -49,6 +56,19 @@ def perturb(theta, dtype, offset, seed, step, k, eps, rounds=DEFAULT_ROUNDS):
     return f32_to_bf16(bf16_to_f32(theta) + delta)
 
 
+def perturb2(theta, dtype, offset, seed, step, k_a, eps_a, k_b, eps_b, rounds=DEFAULT_ROUNDS):
+    """Return theta + (eps_a z_{k_a} + eps_b z_{k_b}), the pair's sum rounded to fp32 first."""
+    theta = _check_theta(theta, dtype)
+    n = theta.shape[0]
+    ea, eb = np.float32(eps_a), np.float32(eps_b)
+    da = np.where(signs(offset, n, seed, step, k_a, rounds) > 0, ea, -ea).astype(np.float32)
+    db = np.where(signs(offset, n, seed, step, k_b, rounds) > 0, eb, -eb).astype(np.float32)
+    d = (da + db).astype(np.float32)
+    if dtype == "f32":
+        return (theta + d).astype(np.float32)
+    return f32_to_bf16(bf16_to_f32(theta) + d)
+
+
 def probe_sum(offset, n, seed, step, c, rounds=DEFAULT_ROUNDS, k_base=0):
     """sum_j c[j] * z_{k_base+j} over the window, in float64 (c taken as float32 values)."""
     c64 = np.asarray(c, dtype=np.float32).astype(np.float64)
@@ -67,6 +87,20 @@ def update(theta, dtype, offset, seed, step, c, lr, rounds=DEFAULT_ROUNDS, k_bas
     if dtype == "f32":
         return f64_to_f32(theta.astype(np.float64) - lr64 * acc)
     return f64_to_bf16(bf16_to_f64(theta) - lr64 * acc)
+
+
+def update_restore(theta, dtype, offset, seed, step, c, lr, k_restore, eps_restore,
+                   rounds=DEFAULT_ROUNDS, k_base=0):
+    """Return round(theta + eps_r z_{k_restore} - lr * sum_j c[j] z_{k_base+j}), rounded once."""
+    theta = _check_theta(theta, dtype)
+    n = theta.shape[0]
+    acc = probe_sum(offset, n, seed, step, c, rounds, k_base)
+    er = np.float64(np.float32(eps_restore))
+    rz = er * signs(offset, n, seed, step, k_restore, rounds)
+    lr64 = np.float64(np.float32(lr))
+    if dtype == "f32":
+        return f64_to_f32((theta.astype(np.float64) + rz) - lr64 * acc)
+    return f64_to_bf16((bf16_to_f64(theta) + rz) - lr64 * acc)
 
 
 def perturb_schedule(theta, dtype, offset, seed, step, k, eps, rounds=DEFAULT_ROUNDS):
