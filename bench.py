@@ -8,6 +8,9 @@ timed region starts; K = 16, eps = lr = 1e-3.
 
 Prints one JSON line. `value` is the step's effective HBM bandwidth: algorithmic bytes
 (one read and one write of every weight per sweep, 3K + 1 sweeps) over the step time.
+`fused_schedule` times the same step in 2K + 1 sweeps (zo_perturb2 merges the restore of
+probe k with the +eps of probe k + 1, zo_update_restore merges the last restore with the
+update) over the same number of steps.
 Per-kernel durations come from HIP events recorded around every launch on the stream the
 kernels run on; `roofline` is the dominant kernel's (zo_perturb: 3K of the 3K + 1 sweeps)
 and `roofline_update` the fused update's.
@@ -149,6 +152,16 @@ def main():
         else:
             zo.zo_update(theta, c, w.lr, seed, step, stream=stream)
 
+    def fused_step(step):
+        lp, lm, l0 = workloads.synthetic_losses(K, step)
+        zo.zo_perturb(theta, 0, w.eps, seed, step, stream=stream)
+        for k in range(K):
+            zo.zo_perturb(theta, k, -2.0 * w.eps, seed, step, stream=stream)
+            if k + 1 < K:
+                zo.zo_perturb2(theta, k, w.eps, k + 1, w.eps, seed, step, stream=stream)
+        c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
+        zo.zo_update_restore(theta, c, w.lr, seed, step, K - 1, w.eps, stream=stream)
+
     for s in range(args.warmup):
         one_step(s, False)
         torch.cuda.synchronize()
@@ -160,6 +173,15 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     log(f"timed {args.steps} steps in {elapsed:.3f} s")
+
+    fused_step(args.warmup + args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        fused_step(args.warmup + args.steps + 1 + s)
+    torch.cuda.synchronize()
+    fused_elapsed = time.perf_counter() - t0
+    log(f"timed {args.steps} fused-schedule steps in {fused_elapsed:.3f} s")
 
     ms = {k: np.array([a.elapsed_time(z) for a, z in v]) for k, v in ev.items()}
     t_step = elapsed / args.steps
@@ -200,6 +222,13 @@ def main():
         "step_params_probes_per_s": float(f"{n * 4 * K / t_step:.4e}"),
         "roofline": roof("zo_perturb", p_ms, p_gbps),
         "roofline_update": roof("zo_update", u_ms, u_gbps),
+        "fused_schedule": {
+            "ms_per_step": round(fused_elapsed / args.steps * 1e3, 3),
+            "sweeps_per_step": 2 * K + 1,
+            "effective_gbps": round((2 * K + 1) * sweep_bytes / (fused_elapsed / args.steps) / 1e9, 1),
+            "speedup_vs_sequential": round(elapsed / fused_elapsed, 3),
+            "step_params_probes_per_s": float(f"{n * 4 * K / (fused_elapsed / args.steps):.4e}"),
+        },
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")

@@ -93,8 +93,9 @@ int zo_probe_coeffs_ex(const double* L_plus, const double* L_minus, uint32_t K, 
  * The fused form of section 4.2 (Eq. 6, Delta theta = -eta Z W Delta l) and of
  * Algorithm 1's per-probe loop: one read and one write of theta for all K probes, which
  * are regenerated in registers. c: host array of K floats (from zo_probe_coeffs).
- * Arithmetic: per element, sum_k c[k] z_k in fp32 (pairwise over each group of 8 probes,
- * pairwise or compensated across groups), s = fl(lr * sum), theta - s in fp32, then one
+ * Arithmetic: per element, sum_k c[k] z_k in fp32 (pairwise within each group of 8 probes,
+ * sequential across groups within runs of 8 groups, compensated across runs),
+ * s = fl(lr * sum), theta - s in fp32, then one
  * rounding to bf16 for bf16 weights. With K = 1 this equals zo_perturb(k = 0,
  * eps = -fl(lr * c[0])) bit for bit.
  * Errors: ZO_ERR_NULL (params NULL with n > 0, c NULL with K > 0), ZO_ERR_ARG (dtype,
@@ -112,6 +113,33 @@ int zo_update(void* params, zo_dtype dtype, uint64_t n, uint64_t seed, uint32_t 
 int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
                  uint32_t step, uint32_t k_base, uint32_t K, const float* c, float lr,
                  void* stream);
+
+/*
+ * zo_perturb2 -- theta[i] <- theta[i] + (eps_a z_{k_a}[offset+i] + eps_b z_{k_b}[offset+i]),
+ * one sweep. On one device Algorithm 1's restore of probe k (+eps) and the +eps of probe
+ * k + 1 are consecutive applications; this applies the pair in one pass, so a step needs
+ * 2K + 1 sweeps instead of 3K + 1. Arithmetic: d = fl32(eps_a z_a + eps_b z_b) (exact when
+ * |eps_a| = |eps_b|), one fp32 addition theta + d, then one rounding to bf16 for bf16
+ * weights; bit-exact and independent of launch shape. k_a may equal k_b; eps_b = 0 gives
+ * exactly zo_perturb(k_a, eps_a).
+ * Errors: as zo_perturb (ZO_ERR_NONFINITE for a non-finite eps_a or eps_b).
+ */
+int zo_perturb2(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
+                uint32_t step, uint32_t k_a, float eps_a, uint32_t k_b, float eps_b, void* stream);
+
+/*
+ * zo_update_restore -- theta[i] <- theta[i] + eps_restore z_{k_restore}[offset+i]
+ *                                  - lr * sum_j c[j] z_{k_base+j}[offset+i], one sweep:
+ * the last probe's restore merged with the fused update (Algorithm 1's final +eps and its
+ * rank-0 update loop; section 4.2, Eq. 6). Arithmetic per element in fp32:
+ * t = fl(theta + eps_restore z), then t - fl(lr * sum) as in zo_update, then one rounding to
+ * bf16 for bf16 weights. eps_restore = 0 gives zo_update_ex's result bit for bit.
+ * Errors: as zo_update_ex (ZO_ERR_NONFINITE also for a non-finite eps_restore). With K = 0
+ * it applies the restore alone.
+ */
+int zo_update_restore(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
+                      uint32_t step, uint32_t k_base, uint32_t K, const float* c, float lr,
+                      uint32_t k_restore, float eps_restore, void* stream);
 
 /*
  * zo_gen_bits -- writes the raw 16-byte probe block of each tile tile_begin ..

@@ -10,6 +10,9 @@ the C names of include/zo.h:
   zo_probe_coeffs_ex(..., alpha, lambda_reg)            also c64, curvature, weight
   zo_update(theta, c, lr, seed, step)                   theta <- theta - lr sum_k c_k z_k
   zo_update_ex(theta, c, lr, seed, step, offset, k_base)
+  zo_perturb2(theta, k_a, eps_a, k_b, eps_b, seed, step) theta + eps_a z_a + eps_b z_b (one pass)
+  zo_update_restore(theta, c, lr, seed, step, k_restore, eps_restore)
+                                                        restore of one probe fused with the update
   zo_gen_bits(out, tile_begin, seed, step, group)       raw probe blocks (uint8 tensor)
 
 If libzo.so has not been built the import succeeds but every call raises ZoLibraryMissing:
@@ -29,8 +32,8 @@ ZO_OK, ZO_ERR_NULL, ZO_ERR_ARG, ZO_ERR_NONFINITE, ZO_ERR_HIP = 0, -1, -2, -3, -4
 ZO_K_MAX = 256
 TILE = 16
 
-EXPORTS = ("zo_perturb", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update", "zo_update_ex",
-           "zo_gen_bits", "zo_strerror", "zo_set_max_blocks", "zo_version")
+EXPORTS = ("zo_perturb", "zo_perturb2", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update", "zo_update_ex",
+           "zo_update_restore", "zo_gen_bits", "zo_strerror", "zo_set_max_blocks", "zo_version")
 
 
 class ZoLibraryMissing(RuntimeError):
@@ -59,14 +62,16 @@ def _lib():
         lib.zo_probe_coeffs_ex.argtypes = [pd, pd, u32, f64, f64, f64, f64, pf, pd, pd, pd]
         lib.zo_update.argtypes = [vp, ctypes.c_int, u64, u64, u32, u32, pf, f32, vp]
         lib.zo_update_ex.argtypes = [vp, ctypes.c_int, u64, u64, u64, u32, u32, u32, pf, f32, vp]
+        lib.zo_perturb2.argtypes = [vp, ctypes.c_int, u64, u64, u64, u32, u32, f32, u32, f32, vp]
+        lib.zo_update_restore.argtypes = [vp, ctypes.c_int, u64, u64, u64, u32, u32, u32, pf, f32, u32, f32, vp]
         lib.zo_gen_bits.argtypes = [vp, u64, u64, u64, u32, u32, vp]
         lib.zo_strerror.argtypes = [ctypes.c_int]
         lib.zo_strerror.restype = ctypes.c_char_p
         lib.zo_set_max_blocks.argtypes = [u32]
         lib.zo_set_max_blocks.restype = None
         lib.zo_version.restype = ctypes.c_char_p
-        for name in ("zo_perturb", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update", "zo_update_ex",
-                     "zo_gen_bits"):
+        for name in ("zo_perturb", "zo_perturb2", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update",
+                     "zo_update_ex", "zo_update_restore", "zo_gen_bits"):
             getattr(lib, name).restype = ctypes.c_int
         _LIB = lib
     return _LIB
@@ -109,6 +114,22 @@ def zo_perturb(theta, k, eps, seed, step, offset=0, stream=None):
     """theta[i] <- theta[i] + eps * z_k[offset + i], in place, asynchronously on the stream."""
     p, dt, n = _theta_args(theta)
     _check(_lib().zo_perturb(p, dt, offset, n, seed, step, k, eps, _stream(theta, stream)), "zo_perturb")
+
+
+def zo_perturb2(theta, k_a, eps_a, k_b, eps_b, seed, step, offset=0, stream=None):
+    """theta[i] <- theta[i] + (eps_a z_{k_a} + eps_b z_{k_b})[offset + i], one pass, in place."""
+    p, dt, n = _theta_args(theta)
+    _check(_lib().zo_perturb2(p, dt, offset, n, seed, step, k_a, eps_a, k_b, eps_b, _stream(theta, stream)),
+           "zo_perturb2")
+
+
+def zo_update_restore(theta, c, lr, seed, step, k_restore, eps_restore, offset=0, k_base=0, stream=None):
+    """theta <- theta + eps_restore z_{k_restore} - lr * sum_j c[j] z_{k_base+j}, one pass, in place."""
+    p, dt, n = _theta_args(theta)
+    c = np.ascontiguousarray(np.asarray(c, dtype=np.float32))
+    cp = c.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if c.size else None
+    _check(_lib().zo_update_restore(p, dt, offset, n, seed, step, k_base, c.size, cp, lr, k_restore, eps_restore,
+                                    _stream(theta, stream)), "zo_update_restore")
 
 
 def zo_update_ex(theta, c, lr, seed, step, offset=0, k_base=0, stream=None):

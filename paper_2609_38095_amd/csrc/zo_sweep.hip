@@ -239,11 +239,19 @@ __device__ __forceinline__ uint64_t edge_tile(const Plan& pl, uint64_t j) {
 }
 
 // ---------------------------------------------------------------------------------------
-// perturb: theta + eps * z_k (bit k mod 8 of each probe byte of group k / 8).
-template <class S>
-__global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* params, Plan pl, Gen gen,
-                                                        uint32_t group, uint32_t bit, float eps) {
+// perturb: theta + eps * z_k (bit k mod 8 of each probe byte of group k / 8). TWO: the
+// fused transition theta + (eps_a z_a + eps_b z_b), the pair's sum rounded to fp32 first.
+struct Probe {
+  uint32_t group, bit;
+  float eps;
+  __device__ __forceinline__ float delta(uint32_t byte) const { return ((byte >> bit) & 1u) ? eps : -eps; }
+};
+
+template <class S, bool TWO>
+__global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* params, Plan pl, Gen gen, Probe a,
+                                                        Probe b) {
   const uint32_t lane = threadIdx.x & 63u;
+  const bool shared_group = a.group == b.group;
   const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
   for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
        c += n_waves) {
@@ -253,14 +261,28 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* pa
     u32x4 d[kU];
 #pragma unroll
     for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
-    uint32_t W[kU][S::kWords];
-    chunk_words(gen, vbase, lane, group, W, S());
+    uint32_t Wa[kU][S::kWords], Wb[kU][S::kWords];
+    chunk_words(gen, vbase, lane, a.group, Wa, S());
+    if (TWO) {
+      if (shared_group) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+#pragma unroll
+          for (int q = 0; q < S::kWords; ++q) Wb[u][q] = Wa[u][q];
+      } else {
+        chunk_words(gen, vbase, lane, b.group, Wb, S());
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       float v[S::kVecElems];
       S::unpack(d[u], v);
 #pragma unroll
-      for (int e = 0; e < S::kVecElems; ++e) v[e] += ((elem_byte<S>(W[u], e) >> bit) & 1u) ? eps : -eps;
+      for (int e = 0; e < S::kVecElems; ++e) {
+        float dv = a.delta(elem_byte<S>(Wa[u], e));
+        if (TWO) dv = dv + b.delta(elem_byte<S>(Wb[u], e));
+        v[e] = v[e] + dv;
+      }
       d[u] = S::pack(v);
     }
 #pragma unroll
@@ -270,10 +292,13 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* pa
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
   for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
     const uint64_t t = edge_tile(pl, j);
-    const uint4 r = gen.block(t, group);
-    const uint32_t x[4] = {r.x, r.y, r.z, r.w};
+    const uint4 ra = gen.block(t, a.group);
+    const uint4 rb = TWO ? gen.block(t, b.group) : ra;
+    const uint32_t xa[4] = {ra.x, ra.y, ra.z, ra.w}, xb[4] = {rb.x, rb.y, rb.z, rb.w};
     tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) {
-      return v + (((word_byte(x[e >> 2], e & 3) >> bit) & 1u) ? eps : -eps);
+      float dv = a.delta(word_byte(xa[e >> 2], e & 3));
+      if (TWO) dv = dv + b.delta(word_byte(xb[e >> 2], e & 3));
+      return v + dv;
     });
   }
 }
@@ -304,12 +329,15 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
   __syncthreads();
 }
 
-// acc[u][e] (+)= table value of group g for each element of the chunk.
-template <class S, bool FIRST>
+// acc[u][e] (+)= table value of group g for each element of the chunk; on_words(g, W) sees
+// the group's generator words.
+template <class S, bool FIRST, class OnWords>
 __device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
-                                          uint64_t vbase, uint32_t lane, uint32_t g, uint32_t g_first) {
+                                          uint64_t vbase, uint32_t lane, uint32_t g, uint32_t g_first,
+                                          OnWords& on_words) {
   uint32_t W[kU][S::kWords];
   chunk_words(gen, vbase, lane, g_first + g, W, S());
+  on_words(g, W);
   const float* tg = tab + 256u * g;
 #pragma unroll
   for (int u = 0; u < kU; ++u)
@@ -322,20 +350,21 @@ __device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const 
 
 // Sum of the tables of groups 0 .. n_groups-1 for the chunk: NG > 0 fixes the count at
 // compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
-template <class S, int NG>
+template <class S, int NG, class OnWords>
 __device__ __forceinline__ void chunk_sums(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
-                                           uint64_t vbase, uint32_t lane, uint32_t n_groups, uint32_t g_first) {
+                                           uint64_t vbase, uint32_t lane, uint32_t n_groups, uint32_t g_first,
+                                           OnWords& on_words) {
   if constexpr (NG > 0) {
-    add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first);
+    add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first, on_words);
 #pragma unroll
-    for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first);
+    for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first, on_words);
   } else {
     float comp[kU][S::kVecElems];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
       float part[kU][S::kVecElems];
-      add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first);
+      add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first, on_words);
       const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
-      for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first);
+      for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first, on_words);
 #pragma unroll
       for (int u = 0; u < kU; ++u)
 #pragma unroll
@@ -391,16 +420,21 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
   }
 }
 
-template <class S, int NG>
+// RESTORE: theta + eps_r z_r - lr * sum (the last probe's restore merged with the update):
+// t = fl(theta + delta_r), then t - fl(lr * sum). The restore probe's words are taken from the
+// group loop when its group is among the update's groups, else generated separately.
+template <class S, int NG, bool RESTORE>
 __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* params, Plan pl, Gen gen,
                                                        uint32_t k_base, uint32_t K, uint32_t n_groups, Coefs cf,
-                                                       float lr) {
+                                                       float lr, Probe r) {
   // n_groups x 256 floats: static for a fixed group count (constant LDS offsets), else dynamic.
   extern __shared__ float tab_dyn[];
   __shared__ float tab_fix[NG > 0 ? NG * 256 : 1];
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   build_tables(tab, cf, k_base, K, n_groups);
   const uint32_t g_first = k_base / 8;
+  const uint32_t rg = r.group - g_first;  // wraps past n_groups when outside the update's groups
+  const bool r_inside = RESTORE && r.group >= g_first && rg < n_groups;
   const uint32_t lane = threadIdx.x & 63u;
   const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
   for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
@@ -412,13 +446,31 @@ __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* par
 #pragma unroll
     for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
     float acc[kU][S::kVecElems];
-    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
+    float rd[kU][S::kVecElems];
+    auto take_restore = [&](const uint32_t (&W)[kU][S::kWords]) {
+#pragma unroll
+      for (int u = 0; u < kU; ++u)
+#pragma unroll
+        for (int e = 0; e < S::kVecElems; ++e) rd[u][e] = r.delta(elem_byte<S>(W[u], e));
+    };
+    auto on_words = [&](uint32_t g, const uint32_t (&W)[kU][S::kWords]) {
+      if (RESTORE && r_inside && g == rg) take_restore(W);
+    };
+    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first, on_words);
+    if (RESTORE && !r_inside) {
+      uint32_t W[kU][S::kWords];
+      chunk_words(gen, vbase, lane, r.group, W, S());
+      take_restore(W);
+    }
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       float v[S::kVecElems];
       S::unpack(d[u], v);
 #pragma unroll
-      for (int e = 0; e < S::kVecElems; ++e) v[e] = v[e] - lr * acc[u][e];
+      for (int e = 0; e < S::kVecElems; ++e) {
+        if (RESTORE) v[e] = v[e] + rd[u][e];
+        v[e] = v[e] - lr * acc[u][e];
+      }
       d[u] = S::pack(v);
     }
 #pragma unroll
@@ -430,7 +482,12 @@ __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* par
     const uint64_t t = edge_tile(pl, j);
     float acc[kTile];
     tile_sums(acc, tab, gen, t, n_groups, g_first);
-    tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) { return v - lr * acc[e]; });
+    const uint4 rr = RESTORE ? gen.block(t, r.group) : make_uint4(0, 0, 0, 0);
+    const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
+    tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) {
+      if (RESTORE) v = v + r.delta(word_byte(xr[e >> 2], e & 3));
+      return v - lr * acc[e];
+    });
   }
 }
 
@@ -503,29 +560,43 @@ uint32_t plan_grid(const Plan& pl) {
 
 int launch_status() { return hipGetLastError() == hipSuccess ? ZO_OK : ZO_ERR_HIP; }
 
-template <class S>
-void launch_perturb(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k, float eps,
-                    hipStream_t st) {
-  const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
-  perturb_kernel<S><<<dim3(plan_grid(pl)), dim3(kBlock), 0, st>>>(static_cast<typename S::storage*>(params), pl,
-                                                                   gen, k / 8, k % 8, eps);
-}
+Probe make_probe(uint32_t k, float eps) { return Probe{k / 8, k % 8, eps}; }
 
 template <class S>
-void launch_update(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k_base, uint32_t K,
-                   uint32_t n_groups, const Coefs& cf, float lr, hipStream_t st) {
+void launch_perturb(void* params, uint64_t offset, uint64_t n, const Gen& gen, const Probe& a, const Probe* b,
+                    hipStream_t st) {
+  const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
+  auto* p = static_cast<typename S::storage*>(params);
+  if (b)
+    perturb_kernel<S, true><<<dim3(plan_grid(pl)), dim3(kBlock), 0, st>>>(p, pl, gen, a, *b);
+  else
+    perturb_kernel<S, false><<<dim3(plan_grid(pl)), dim3(kBlock), 0, st>>>(p, pl, gen, a, a);
+}
+
+template <class S, bool RESTORE>
+void launch_update_r(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k_base, uint32_t K,
+                     uint32_t n_groups, const Coefs& cf, float lr, const Probe& r, hipStream_t st) {
   const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
   const dim3 grid(plan_grid(pl)), block(kBlock);
   const bool fixed = n_groups == 1 || n_groups == 2 || n_groups == 4 || n_groups == 8;
   const size_t lds = fixed ? 0 : static_cast<size_t>(n_groups) * 256 * sizeof(float);
   auto* p = static_cast<typename S::storage*>(params);
   switch (n_groups) {
-    case 1: update_kernel<S, 1><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
-    case 2: update_kernel<S, 2><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
-    case 4: update_kernel<S, 4><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
-    case 8: update_kernel<S, 8><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
-    default: update_kernel<S, 0><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr); break;
+    case 1: update_kernel<S, 1, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
+    case 2: update_kernel<S, 2, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
+    case 4: update_kernel<S, 4, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
+    case 8: update_kernel<S, 8, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
+    default: update_kernel<S, 0, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
   }
+}
+
+template <class S>
+void launch_update(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k_base, uint32_t K,
+                   uint32_t n_groups, const Coefs& cf, float lr, const Probe* r, hipStream_t st) {
+  if (r)
+    launch_update_r<S, true>(params, offset, n, gen, k_base, K, n_groups, cf, lr, *r, st);
+  else
+    launch_update_r<S, false>(params, offset, n, gen, k_base, K, n_groups, cf, lr, Probe{0, 0, 0.0f}, st);
 }
 
 Gen make_gen(uint64_t seed, uint32_t step) {
@@ -534,37 +605,38 @@ Gen make_gen(uint64_t seed, uint32_t step) {
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-int zo_perturb(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
-               uint32_t k, float eps, void* stream) {
+int perturb_impl(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+                 const Probe& a, const Probe* b, void* stream) {
   size_t elem = 0;
   const int rc = check_params(params, dtype, offset, n, &elem);
   if (rc != ZO_OK) return rc;
-  if (!std::isfinite(eps)) return ZO_ERR_NONFINITE;
+  if (!std::isfinite(a.eps) || (b && !std::isfinite(b->eps))) return ZO_ERR_NONFINITE;
   if (n == 0) return ZO_OK;
   const Gen gen = make_gen(seed, step);
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   if (dtype == ZO_F32)
-    launch_perturb<F32>(params, offset, n, gen, k, eps, st);
+    launch_perturb<F32>(params, offset, n, gen, a, b, st);
   else
-    launch_perturb<BF16>(params, offset, n, gen, k, eps, st);
+    launch_perturb<BF16>(params, offset, n, gen, a, b, st);
   return launch_status();
 }
 
-int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
-                 uint32_t k_base, uint32_t K, const float* c, float lr, void* stream) {
+int update_impl(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+                uint32_t k_base, uint32_t K, const float* c, float lr, const Probe* r, void* stream) {
   size_t elem = 0;
   const int rc = check_params(params, dtype, offset, n, &elem);
   if (rc != ZO_OK) return rc;
   if (K > ZO_K_MAX) return ZO_ERR_ARG;
   if (static_cast<uint64_t>(k_base) + K > (1ull << 32)) return ZO_ERR_ARG;
   if (K > 0 && c == nullptr) return ZO_ERR_NULL;
-  if (!std::isfinite(lr)) return ZO_ERR_NONFINITE;
+  if (!std::isfinite(lr) || (r && !std::isfinite(r->eps))) return ZO_ERR_NONFINITE;
   for (uint32_t j = 0; j < K; ++j)
     if (!std::isfinite(c[j])) return ZO_ERR_NONFINITE;
-  if (n == 0 || K == 0) return ZO_OK;
+  if (n == 0) return ZO_OK;
+  if (K == 0) return r ? perturb_impl(params, dtype, offset, n, seed, step, *r, nullptr, stream) : ZO_OK;
   Coefs cf;
   for (uint32_t j = 0; j < ZO_K_MAX; ++j) cf.c[j] = j < K ? c[j] : 0.0f;
   const uint32_t g_first = k_base / 8;
@@ -574,15 +646,42 @@ int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   if (dtype == ZO_F32)
-    launch_update<F32>(params, offset, n, gen, k_base, K, n_groups, cf, lr, st);
+    launch_update<F32>(params, offset, n, gen, k_base, K, n_groups, cf, lr, r, st);
   else
-    launch_update<BF16>(params, offset, n, gen, k_base, K, n_groups, cf, lr, st);
+    launch_update<BF16>(params, offset, n, gen, k_base, K, n_groups, cf, lr, r, st);
   return launch_status();
+}
+
+}  // namespace
+
+extern "C" {
+
+int zo_perturb(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+               uint32_t k, float eps, void* stream) {
+  return perturb_impl(params, dtype, offset, n, seed, step, make_probe(k, eps), nullptr, stream);
+}
+
+int zo_perturb2(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+                uint32_t k_a, float eps_a, uint32_t k_b, float eps_b, void* stream) {
+  const Probe b = make_probe(k_b, eps_b);
+  return perturb_impl(params, dtype, offset, n, seed, step, make_probe(k_a, eps_a), &b, stream);
+}
+
+int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+                 uint32_t k_base, uint32_t K, const float* c, float lr, void* stream) {
+  return update_impl(params, dtype, offset, n, seed, step, k_base, K, c, lr, nullptr, stream);
 }
 
 int zo_update(void* params, zo_dtype dtype, uint64_t n, uint64_t seed, uint32_t step, uint32_t K,
               const float* c, float lr, void* stream) {
-  return zo_update_ex(params, dtype, 0, n, seed, step, 0, K, c, lr, stream);
+  return update_impl(params, dtype, 0, n, seed, step, 0, K, c, lr, nullptr, stream);
+}
+
+int zo_update_restore(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+                      uint32_t k_base, uint32_t K, const float* c, float lr, uint32_t k_restore,
+                      float eps_restore, void* stream) {
+  const Probe r = make_probe(k_restore, eps_restore);
+  return update_impl(params, dtype, offset, n, seed, step, k_base, K, c, lr, &r, stream);
 }
 
 int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_t seed, uint32_t step,

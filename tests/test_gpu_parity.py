@@ -253,6 +253,109 @@ def test_empty_and_noop_calls():
     assert torch.equal(u, before)
 
 
+# ----------------------------------------------------------------------------- fused transitions
+PERTURB2_CASES = [
+    # n, offset, k_a, e_a, k_b, e_b
+    (1000, 0, 3, 1e-3, 4, 1e-3), (70_001, 0, 7, 1e-3, 8, 1e-3), (4099, 2 ** 35 + 7, 0, 1e-3, 1, 1e-3),
+    (5000, 3, 5, 1e-3, 5, 1e-3), (5000, 0, 5, 1e-3, 5, -1e-3), (20_000, 0, 9, 1e-3, 100, -3.7e-4),
+    (3000, 16, 2, -2e-3, 2, 0.0), (17, 0, 1, 1e-3, 2, 1e-3),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,offset,k_a,e_a,k_b,e_b", PERTURB2_CASES)
+def test_perturb2_bit_exact(dtype, n, offset, k_a, e_a, k_b, e_b):
+    note(f"perturb2 {dtype} n {n} offset {offset} ({k_a}, {e_a}) ({k_b}, {e_b})")
+    seed, step = 77, 9
+    if dtype == "f32":
+        th = workloads.normal_f32(n, 2)
+        t = to_dev_f32(th)
+        zo.zo_perturb2(t, k_a, e_a, k_b, e_b, seed, step, offset=offset)
+        want = oracle.perturb2(th, "f32", offset, seed, step, k_a, e_a, k_b, e_b)
+        np.testing.assert_array_equal(t.cpu().numpy(), want)
+    else:
+        th = workloads.normal_bf16_bits(n, 2)
+        t = to_dev_bf16(th)
+        zo.zo_perturb2(t, k_a, e_a, k_b, e_b, seed, step, offset=offset)
+        np.testing.assert_array_equal(host_bits(t), oracle.perturb2(th, "bf16", offset, seed, step, k_a, e_a, k_b, e_b))
+
+
+def test_perturb2_zero_second_scale_equals_perturb():
+    bits = workloads.normal_bf16_bits(100_003, 3)
+    a, b = to_dev_bf16(bits), to_dev_bf16(bits)
+    zo.zo_perturb2(a, 6, 1e-3, 13, 0.0, 5, 5)
+    zo.zo_perturb(b, 6, 1e-3, 5, 5)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def assert_restore_update_close(got, want, theta, c, lr, er, dtype):
+    th64 = theta.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(theta)
+    g64 = got.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(got)
+    w64 = want.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(want)
+    scale = np.maximum(np.maximum(np.abs(th64) + abs(er), np.abs(w64)), abs(lr) * np.abs(np.asarray(c, np.float64)).sum())
+    allow = 1e-6 * scale
+    if dtype == "bf16":
+        allow = allow + bf16_spacing(np.maximum(np.abs(g64), np.abs(w64)))
+    err = np.abs(g64 - w64)
+    assert np.all(err <= allow), f"{np.count_nonzero(err > allow)} elements out of bound"
+
+
+RESTORE_CASES = [
+    # n, offset, k_base, K, k_restore
+    (50_000, 0, 0, 16, 15), (20_000, 5, 0, 4, 3), (30_000, 0, 0, 64, 63), (9_000, 2 ** 33, 0, 200, 199),
+    (10_000, 0, 0, 16, 40), (10_000, 0, 8, 16, 0), (7_000, 0, 3, 13, 15), (5_000, 0, 0, 0, 2),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,offset,k_base,K,k_restore", RESTORE_CASES)
+def test_update_restore_matches_oracle(dtype, n, offset, k_base, K, k_restore):
+    note(f"update_restore {dtype} n {n} offset {offset} k_base {k_base} K {K} restore {k_restore}")
+    seed, step, lr, er = 31, 4, 1e-3, 1e-3
+    c = np.random.default_rng(K + 1).standard_normal(K).astype(np.float32) * 3
+    th = workloads.normal_f32(n, 3) if dtype == "f32" else workloads.normal_bf16_bits(n, 3)
+    t = to_dev_f32(th) if dtype == "f32" else to_dev_bf16(th)
+    zo.zo_update_restore(t, c, lr, seed, step, k_restore, er, offset=offset, k_base=k_base)
+    got = t.cpu().numpy() if dtype == "f32" else host_bits(t)
+    want = oracle.update_restore(th, dtype, offset, seed, step, c, lr, k_restore, er, k_base=k_base)
+    assert_restore_update_close(got, want, th, c, lr, er, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_update_restore_zero_restore_equals_update(dtype):
+    base = workloads.normal_f32(100_003, 4)
+    c = np.random.default_rng(2).standard_normal(16).astype(np.float32)
+    if dtype == "f32":
+        a, b = to_dev_f32(base), to_dev_f32(base)
+    else:
+        bits = oracle.f32_to_bf16(base)
+        a, b = to_dev_bf16(bits), to_dev_bf16(bits)
+    zo.zo_update_restore(a, c, 1e-3, 6, 6, 15, 0.0)
+    zo.zo_update(b, c, 1e-3, 6, 6)
+    view = (lambda x: x.view(torch.int16)) if dtype == "bf16" else (lambda x: x)
+    assert torch.equal(view(a), view(b))
+
+
+def test_full_tiny_step_fused():
+    """The tiny workload in 2K + 1 sweeps: +eps z_0; per probe -2 eps z_k then the merged
+    restore / next +eps; the last restore merged with the update."""
+    w = workloads.WORKLOADS["tiny"]
+    K = w.K[0]
+    th = workloads.tiny_theta(w.n)
+    lp, lm, l0 = workloads.synthetic_losses(K, 1)
+    t = to_dev_f32(th)
+    zo.zo_perturb(t, 0, w.eps, 0, 0)
+    for k in range(K):
+        zo.zo_perturb(t, k, -2 * w.eps, 0, 0)
+        if k + 1 < K:
+            zo.zo_perturb2(t, k, w.eps, k + 1, w.eps, 0, 0)
+    c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
+    zo.zo_update_restore(t, c, w.lr, 0, 0, K - 1, w.eps)
+    want, co, _ = oracle.full_step_fused(th, "f32", 0, 0, 0, w.eps, w.lr, lp, lm, l0)
+    np.testing.assert_array_equal(c, co["c"])
+    assert_f32_update_close(t.cpu().numpy(), want, c, w.lr)
+
+
 # ----------------------------------------------------------------------------- full step
 def test_full_tiny_step():
     """The tiny fp32 workload: 2^20 weights, K = 4, eps 1e-3, lr 1e-4 (schedule + coeffs + update)."""
@@ -301,9 +404,16 @@ def test_full_size_sampled_windows(name, K):
     c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
     zo.zo_update(buf, c, w.lr, seed, step)
     after = grab()
+    zo.zo_perturb2(buf, 5, w.eps, 6, w.eps, seed, step)
+    trans = grab()
+    zo.zo_update_restore(buf, c, w.lr, seed, step, 6, w.eps)
+    final = grab()
     torch.cuda.synchronize()
     del buf
     torch.cuda.empty_cache()
-    for s, b, m, a in zip(wins, before, mid, after):
+    for s, b, m, a, tr, f in zip(wins, before, mid, after, trans, final):
         np.testing.assert_array_equal(m, oracle.perturb(b, "bf16", s, seed, step, 5, w.eps))
         assert_bf16_within_1ulp(a, oracle.update(m, "bf16", s, seed, step, c, w.lr), m, c, w.lr)
+        np.testing.assert_array_equal(tr, oracle.perturb2(a, "bf16", s, seed, step, 5, w.eps, 6, w.eps))
+        assert_restore_update_close(f, oracle.update_restore(tr, "bf16", s, seed, step, c, w.lr, 6, w.eps),
+                                    tr, c, w.lr, w.eps, "bf16")
