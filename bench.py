@@ -29,26 +29,29 @@ if ROOT not in sys.path:
 
 METRIC = "fused probe-update effective HBM GB/s + params·probes/s (OPT-13B shape, K=16)"
 HBM_PEAK_GBPS = 8000.0
+# VALU issue peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a wave64 instruction takes 4 cycles).
+VALU_PEAK_TLANEOPS = 256 * 64 * 2.4e9 / 1e12
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def measured_traffic(workload, K, dtype):
-    """HBM bytes per launch from the committed rocprofv3 counter summaries (FETCH_SIZE and
-    WRITE_SIZE, each scaled by a plain copy of known size), keyed by kernel; {} when no
-    summary matches this workload or the sweep source has changed since it was taken."""
+def measured_counters(workload, K, dtype):
+    """Per-launch HBM bytes (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known
+    size) and VALU instruction counts (SQ_INSTS_VALU) from the committed rocprofv3 summaries,
+    keyed by kernel; {} when none matches this workload or the sweep source has changed since
+    the counters were taken."""
     import glob
     import hashlib
     src = os.path.join(ROOT, "paper_2609_38095_amd", "csrc", "zo_sweep.hip")
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*hbm_counters.md"))):
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         for line in open(path):
-            if line.startswith("traffic-json:"):
+            if line.startswith("counters-json:"):
                 d = json.loads(line.split(":", 1)[1])
                 if (d.get("workload"), d.get("K"), d.get("dtype"), d.get("source_sha256")) == (workload, K, dtype, digest):
-                    return d["bytes_per_launch"]
+                    return d
     return {}
 
 
@@ -191,14 +194,24 @@ def main():
     p_ms, u_ms = float(ms["perturb"].mean()), float(ms["update"].mean())
     p_gbps, u_gbps = sweep_bytes / (p_ms * 1e-3) / 1e9, sweep_bytes / (u_ms * 1e-3) / 1e9
 
-    traffic = measured_traffic(w.name, K, w.dtype)
+    counters = measured_counters(w.name, K, w.dtype)
 
     def roof(kernel, avg_ms, gb):
         d = ms["perturb" if kernel == "zo_perturb" else "update"]
-        return {"kernel": kernel, "bound": "hbm", "achieved": round(gb, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(gb / HBM_PEAK_GBPS, 4), "traffic": traffic.get(kernel), "avg_ms": round(avg_ms, 4),
-                "min_ms": round(float(d.min()), 4), "max_ms": round(float(d.max()), 4), "launches": int(d.size),
-                "bytes_per_launch": sweep_bytes}
+        hbm_frac = gb / HBM_PEAK_GBPS
+        valu = counters.get("valu_instructions_per_launch", {}).get(kernel)
+        alu = valu * 64 / (avg_ms * 1e-3) / 1e12 if valu else None
+        r = {"kernel": kernel, "bound": "hbm", "achieved": round(gb, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+             "frac": round(hbm_frac, 4), "traffic": counters.get("traffic_bytes_per_launch", {}).get(kernel),
+             "avg_ms": round(avg_ms, 4), "min_ms": round(float(d.min()), 4), "max_ms": round(float(d.max()), 4),
+             "launches": int(d.size), "bytes_per_launch": sweep_bytes, "hbm_frac": round(hbm_frac, 4)}
+        if alu is not None:
+            r["valu_tlaneops"] = round(alu, 2)
+            r["alu_frac"] = round(alu / VALU_PEAK_TLANEOPS, 4)
+            if alu / VALU_PEAK_TLANEOPS > hbm_frac:
+                r.update(bound="alu", achieved=round(alu, 2), peak=round(VALU_PEAK_TLANEOPS, 2), unit="Tlane-op/s",
+                         frac=round(alu / VALU_PEAK_TLANEOPS, 4))
+        return r
 
     out = {
         "metric": METRIC,

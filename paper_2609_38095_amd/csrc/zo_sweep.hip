@@ -234,6 +234,23 @@ struct Plan {
   uint64_t head_t0, head_nt, tail_t0, tail_nt;
 };
 
+// Byte address of chunk c (global chunk index pl.c_first + c) inside params.
+template <class S>
+__device__ __forceinline__ char* chunk_base(typename S::storage* params, const Plan& pl, uint64_t c) {
+  const uint64_t first_elem = (pl.c_first + c) * ChunkShape<S>::kElems;
+  return reinterpret_cast<char*>(params) + (first_elem - pl.lo) * sizeof(typename S::storage);
+}
+
+__device__ __forceinline__ void load_chunk(u32x4 (&d)[kU], const char* base, uint32_t lane) {
+#pragma unroll
+  for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
+}
+
+__device__ __forceinline__ void store_chunk(char* base, const u32x4 (&d)[kU], uint32_t lane) {
+#pragma unroll
+  for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
+}
+
 __device__ __forceinline__ uint64_t edge_tile(const Plan& pl, uint64_t j) {
   return j < pl.head_nt ? pl.head_t0 + j : pl.tail_t0 + (j - pl.head_nt);
 }
@@ -256,11 +273,9 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* pa
   for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
        c += n_waves) {
     const uint64_t vbase = (pl.c_first + c) * ChunkShape<S>::kVecs;
-    char* base = reinterpret_cast<char*>(params) +
-                 (vbase * S::kVecElems - pl.lo) * sizeof(typename S::storage);
+    char* base = chunk_base<S>(params, pl, c);
     u32x4 d[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
+    load_chunk(d, base, lane);
     uint32_t Wa[kU][S::kWords], Wb[kU][S::kWords];
     chunk_words(gen, vbase, lane, a.group, Wa, S());
     if (TWO) {
@@ -285,8 +300,7 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* pa
       }
       d[u] = S::pack(v);
     }
-#pragma unroll
-    for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
+    store_chunk(base, d, lane);
   }
   const uint64_t n_edge = pl.head_nt + pl.tail_nt;
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
@@ -421,8 +435,8 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 }
 
 // RESTORE: theta + eps_r z_r - lr * sum (the last probe's restore merged with the update):
-// t = fl(theta + delta_r), then t - fl(lr * sum). The restore probe's words are taken from the
-// group loop when its group is among the update's groups, else generated separately.
+// t = fl(theta + delta_r), then t - fl(lr * sum). The restore probe's words are generated
+// after the group loop (reusing the loop's words would keep them live across it).
 template <class S, int NG, bool RESTORE>
 __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* params, Plan pl, Gen gen,
                                                        uint32_t k_base, uint32_t K, uint32_t n_groups, Coefs cf,
@@ -433,48 +447,31 @@ __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* par
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   build_tables(tab, cf, k_base, K, n_groups);
   const uint32_t g_first = k_base / 8;
-  const uint32_t rg = r.group - g_first;  // wraps past n_groups when outside the update's groups
-  const bool r_inside = RESTORE && r.group >= g_first && rg < n_groups;
   const uint32_t lane = threadIdx.x & 63u;
   const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
   for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
        c += n_waves) {
     const uint64_t vbase = (pl.c_first + c) * ChunkShape<S>::kVecs;
-    char* base = reinterpret_cast<char*>(params) +
-                 (vbase * S::kVecElems - pl.lo) * sizeof(typename S::storage);
+    char* base = chunk_base<S>(params, pl, c);
     u32x4 d[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
+    load_chunk(d, base, lane);
     float acc[kU][S::kVecElems];
-    float rd[kU][S::kVecElems];
-    auto take_restore = [&](const uint32_t (&W)[kU][S::kWords]) {
-#pragma unroll
-      for (int u = 0; u < kU; ++u)
-#pragma unroll
-        for (int e = 0; e < S::kVecElems; ++e) rd[u][e] = r.delta(elem_byte<S>(W[u], e));
-    };
-    auto on_words = [&](uint32_t g, const uint32_t (&W)[kU][S::kWords]) {
-      if (RESTORE && r_inside && g == rg) take_restore(W);
-    };
-    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first, on_words);
-    if (RESTORE && !r_inside) {
-      uint32_t W[kU][S::kWords];
-      chunk_words(gen, vbase, lane, r.group, W, S());
-      take_restore(W);
-    }
+    auto no_words = [](uint32_t, const uint32_t (&)[kU][S::kWords]) {};
+    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first, no_words);
+    uint32_t Wr[kU][S::kWords];  // the restore probe's generator words
+    if (RESTORE) chunk_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       float v[S::kVecElems];
       S::unpack(d[u], v);
 #pragma unroll
       for (int e = 0; e < S::kVecElems; ++e) {
-        if (RESTORE) v[e] = v[e] + rd[u][e];
+        if (RESTORE) v[e] = v[e] + r.delta(elem_byte<S>(Wr[u], e));
         v[e] = v[e] - lr * acc[u][e];
       }
       d[u] = S::pack(v);
     }
-#pragma unroll
-    for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
+    store_chunk(base, d, lane);
   }
   const uint64_t n_edge = pl.head_nt + pl.tail_nt;
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
