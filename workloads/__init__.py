@@ -113,3 +113,14 @@ def fill_opt_buffer_device(buf, w):
             g = torch.Generator(device=buf.device)
             g.manual_seed(1000 + idx)
             view.normal_(0.0, 0.02, generator=g)
+
+
+def stiff_paraboloid(d, kappa, seed):
+    """The stiff paraboloid J(x) = x^T R^T diag(kappa, 1, ..., 1) R x with a random orthonormal
+    R (section 5.3, appendix A.2), and a starting point x0 ~ N(0, 1) (float32).
+    Returns (A = R^T diag R as float64 [d, d], x0)."""
+    rng = np.random.default_rng(seed)
+    R, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    A = R.T @ np.diag([float(kappa)] + [1.0] * (d - 1)) @ R
+    x0 = rng.standard_normal(d).astype(np.float32)
+    return A, x0
