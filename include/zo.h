@@ -30,7 +30,7 @@
  *     successful no-op.
  *   - No global state is kept between calls except an optional launch-width override
  *     (zo_set_max_blocks); calls on different streams may run concurrently on disjoint
- *     parameter memory.
+ *     parameter memory. The library allocates no device memory.
  */
 #ifndef ZO_H_
 #define ZO_H_
@@ -51,8 +51,17 @@ enum {
   ZO_ERR_HIP = -4        /* the HIP runtime refused the launch */
 };
 
-/* Most probes one zo_update call applies (coefficients travel as kernel arguments). */
-#define ZO_K_MAX 256u
+/* Most probes one zo_update call applies (coefficients travel as kernel arguments, 4 KiB). */
+#define ZO_K_MAX 1024u
+
+/* One tensor of a model's parameters, for the *_segments calls: `params` is caller-owned
+ * device memory (aligned to the element size) holding n elements whose global element
+ * indices are offset .. offset + n - 1. */
+typedef struct {
+  void* params;
+  uint64_t offset;
+  uint64_t n;
+} zo_segment;
 
 /*
  * zo_perturb -- theta[i] <- theta[i] + eps * z_k[offset + i], for i in [0, n).
@@ -100,6 +109,8 @@ int zo_probe_coeffs_ex(const double* L_plus, const double* L_minus, uint32_t K, 
  * eps = -fl(lr * c[0])) bit for bit.
  * Errors: ZO_ERR_NULL (params NULL with n > 0, c NULL with K > 0), ZO_ERR_ARG (dtype,
  * alignment, K > ZO_K_MAX, k_base + K > 2^32), ZO_ERR_NONFINITE (lr or any c[k]), ZO_ERR_HIP.
+ * Cost: one read and one write of theta; above about 24 probes the sweep is bound by the
+ * probe generator (VALU) rather than by HBM.
  */
 int zo_update(void* params, zo_dtype dtype, uint64_t n, uint64_t seed, uint32_t step,
               uint32_t K, const float* c, float lr, void* stream);
@@ -140,6 +151,35 @@ int zo_perturb2(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint6
 int zo_update_restore(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
                       uint32_t step, uint32_t k_base, uint32_t K, const float* c, float lr,
                       uint32_t k_restore, float eps_restore, void* stream);
+
+/*
+ * zo_perturb_segments -- zo_perturb2 over a list of separate tensors (a model that keeps
+ * its parameters in separate allocations rather than one flat buffer): for every segment s,
+ * theta_s[i] <- theta_s[i] + (eps_a z_{k_a} + eps_b z_{k_b})[offset_s + i]. eps_b = 0 is the
+ * one-probe zo_perturb. Each element's result is exactly what zo_perturb / zo_perturb2 give
+ * for that tensor alone. segs: host array of n_segs entries, read during the call.
+ * Segments with n = 0 are skipped; the global index ranges may be in any order but the
+ * segments' memory must not overlap. The tensors are swept in launches of up to 64
+ * segments each (one sweep's worth of HBM traffic in total).
+ * Errors: ZO_ERR_NULL (segs NULL with n_segs > 0, a segment's params NULL with n > 0),
+ * ZO_ERR_ARG (dtype, a misaligned segment, an index range reaching 2^64, overlapping
+ * segments), ZO_ERR_NONFINITE, all before anything is launched; ZO_ERR_HIP if a launch
+ * fails, in which case earlier batches may already be enqueued.
+ */
+int zo_perturb_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed,
+                        uint32_t step, uint32_t k_a, float eps_a, uint32_t k_b, float eps_b,
+                        void* stream);
+
+/*
+ * zo_update_segments -- zo_update_restore over a list of separate tensors (see
+ * zo_perturb_segments for the segment rules): theta_s <- theta_s + eps_restore z_{k_restore}
+ * - lr * sum_j c[j] z_{k_base+j}, each element as zo_update_restore computes it for that
+ * tensor alone; eps_restore = 0 is zo_update_ex. Errors: as zo_perturb_segments, plus those
+ * of zo_update_ex for K, k_base and c.
+ */
+int zo_update_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed,
+                       uint32_t step, uint32_t k_base, uint32_t K, const float* c, float lr,
+                       uint32_t k_restore, float eps_restore, void* stream);
 
 /*
  * zo_gen_bits -- writes the raw 16-byte probe block of each tile tile_begin ..

@@ -13,6 +13,9 @@ the C names of include/zo.h:
   zo_perturb2(theta, k_a, eps_a, k_b, eps_b, seed, step) theta + eps_a z_a + eps_b z_b (one pass)
   zo_update_restore(theta, c, lr, seed, step, k_restore, eps_restore)
                                                         restore of one probe fused with the update
+  zo_perturb_segments(tensors, offsets, k_a, eps_a, k_b, eps_b, seed, step)
+  zo_update_segments(tensors, offsets, c, lr, seed, step, k_restore=0, eps_restore=0.0)
+                                                        the same over a list of separate tensors
   zo_gen_bits(out, tile_begin, seed, step, group)       raw probe blocks (uint8 tensor)
 
 If libzo.so has not been built the import succeeds but every call raises ZoLibraryMissing:
@@ -29,11 +32,16 @@ LIB_PATH = os.path.join(PKG_DIR, "libzo.so")
 
 ZO_F32, ZO_BF16 = 0, 1
 ZO_OK, ZO_ERR_NULL, ZO_ERR_ARG, ZO_ERR_NONFINITE, ZO_ERR_HIP = 0, -1, -2, -3, -4
-ZO_K_MAX = 256
+ZO_K_MAX = 1024
 TILE = 16
 
 EXPORTS = ("zo_perturb", "zo_perturb2", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update", "zo_update_ex",
-           "zo_update_restore", "zo_gen_bits", "zo_strerror", "zo_set_max_blocks", "zo_version")
+           "zo_update_restore", "zo_perturb_segments", "zo_update_segments", "zo_gen_bits", "zo_strerror",
+           "zo_set_max_blocks", "zo_version")
+
+
+class ZoSegment(ctypes.Structure):
+    _fields_ = [("params", ctypes.c_void_p), ("offset", ctypes.c_uint64), ("n", ctypes.c_uint64)]
 
 
 class ZoLibraryMissing(RuntimeError):
@@ -64,6 +72,9 @@ def _lib():
         lib.zo_update_ex.argtypes = [vp, ctypes.c_int, u64, u64, u64, u32, u32, u32, pf, f32, vp]
         lib.zo_perturb2.argtypes = [vp, ctypes.c_int, u64, u64, u64, u32, u32, f32, u32, f32, vp]
         lib.zo_update_restore.argtypes = [vp, ctypes.c_int, u64, u64, u64, u32, u32, u32, pf, f32, u32, f32, vp]
+        ps = ctypes.POINTER(ZoSegment)
+        lib.zo_perturb_segments.argtypes = [ps, u32, ctypes.c_int, u64, u32, u32, f32, u32, f32, vp]
+        lib.zo_update_segments.argtypes = [ps, u32, ctypes.c_int, u64, u32, u32, u32, pf, f32, u32, f32, vp]
         lib.zo_gen_bits.argtypes = [vp, u64, u64, u64, u32, u32, vp]
         lib.zo_strerror.argtypes = [ctypes.c_int]
         lib.zo_strerror.restype = ctypes.c_char_p
@@ -71,7 +82,8 @@ def _lib():
         lib.zo_set_max_blocks.restype = None
         lib.zo_version.restype = ctypes.c_char_p
         for name in ("zo_perturb", "zo_perturb2", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update",
-                     "zo_update_ex", "zo_update_restore", "zo_gen_bits"):
+                     "zo_update_ex", "zo_update_restore", "zo_perturb_segments", "zo_update_segments",
+                     "zo_gen_bits"):
             getattr(lib, name).restype = ctypes.c_int
         _LIB = lib
     return _LIB
@@ -130,6 +142,38 @@ def zo_update_restore(theta, c, lr, seed, step, k_restore, eps_restore, offset=0
     cp = c.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if c.size else None
     _check(_lib().zo_update_restore(p, dt, offset, n, seed, step, k_base, c.size, cp, lr, k_restore, eps_restore,
                                     _stream(theta, stream)), "zo_update_restore")
+
+
+def _segments(tensors, offsets):
+    import torch
+    tensors = list(tensors)
+    if len(tensors) != len(offsets):
+        raise ValueError("one global offset per tensor")
+    dts = {t.dtype for t in tensors}
+    if len(dts) > 1:
+        raise TypeError("all tensors must share one dtype")
+    arr = (ZoSegment * max(len(tensors), 1))()
+    dt = ZO_F32
+    for i, (t, o) in enumerate(zip(tensors, offsets)):
+        p, dt, n = _theta_args(t)
+        arr[i] = ZoSegment(p, int(o), n)
+    return arr, len(tensors), dt, (tensors[0] if tensors else torch.device("cuda"))
+
+
+def zo_perturb_segments(tensors, offsets, k_a, eps_a, k_b, eps_b, seed, step, stream=None):
+    """For each tensor t_s with global offset o_s: t_s <- t_s + (eps_a z_{k_a} + eps_b z_{k_b})[o_s + i]."""
+    arr, n, dt, ref = _segments(tensors, offsets)
+    _check(_lib().zo_perturb_segments(arr, n, dt, seed, step, k_a, eps_a, k_b, eps_b, _stream(ref, stream)),
+           "zo_perturb_segments")
+
+
+def zo_update_segments(tensors, offsets, c, lr, seed, step, k_restore=0, eps_restore=0.0, k_base=0, stream=None):
+    """For each tensor: t_s <- t_s + eps_restore z_{k_restore} - lr * sum_j c[j] z_{k_base+j} (global indices)."""
+    arr, n, dt, ref = _segments(tensors, offsets)
+    c = np.ascontiguousarray(np.asarray(c, dtype=np.float32))
+    cp = c.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if c.size else None
+    _check(_lib().zo_update_segments(arr, n, dt, seed, step, k_base, c.size, cp, lr, k_restore, eps_restore,
+                                     _stream(ref, stream)), "zo_update_segments")
 
 
 def zo_update_ex(theta, c, lr, seed, step, offset=0, k_base=0, stream=None):

@@ -18,6 +18,11 @@
 // (and everything, when the storage is not 16-byte aligned relative to the global index)
 // take an element-wise path, one tile per lane.
 //
+// zo_perturb_segments / zo_update_segments sweep a list of separate tensors: the host validates
+// the list, builds one plan per tensor and launches batches of up to 64 plans (kernel
+// arguments); inside a launch the chunks and edge tiles of all its tensors are numbered
+// consecutively and each wave maps its chunk to a tensor with a forward-only cursor.
+//
 // The update keeps, per probe group, a 256-entry table in LDS: entry b is the signed sum of
 // the group's 8 coefficients selected by the bits of b (pairwise). Applying 8 probes to an
 // element costs a byte extract and an LDS read. Groups accumulate in fp32, sequentially
@@ -27,8 +32,11 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <utility>
+#include <vector>
 
 #include "zo.h"
 
@@ -211,7 +219,8 @@ __device__ __forceinline__ uint32_t elem_byte(const uint32_t (&w)[S::kWords], in
   return word_byte(w[e >> 2], e & 3);
 }
 
-// Element-wise path: elements of tile t inside [lo, hi), one lane.
+// Element-wise path: elements of tile t inside [lo, hi), one lane; params holds global
+// element lo.
 template <class S, class F>
 __device__ __forceinline__ void tile_elementwise(typename S::storage* params, uint64_t lo, uint64_t hi, uint64_t t,
                                                  F f) {
@@ -226,20 +235,25 @@ __device__ __forceinline__ void tile_elementwise(typename S::storage* params, ui
   }
 }
 
-// What a launch covers: global elements [lo, hi); full chunks [c_first, c_first + n_chunks)
-// take the vector path; the remaining edge tiles are [head_t0, +head_nt) and [tail_t0, +tail_nt).
+// One segment: global elements [lo, hi) stored from `base` (the address of global element lo).
+// Full chunks [c_first, c_first + n_chunks) take the vector path; the edge tiles
+// [head_t0, +head_nt) and [tail_t0, +tail_nt) take the element-wise path.
 struct Plan {
+  char* base;
   uint64_t lo, hi;
   uint64_t c_first, n_chunks;
   uint64_t head_t0, head_nt, tail_t0, tail_nt;
 };
 
-// Byte address of chunk c (global chunk index pl.c_first + c) inside params.
-template <class S>
-__device__ __forceinline__ char* chunk_base(typename S::storage* params, const Plan& pl, uint64_t c) {
-  const uint64_t first_elem = (pl.c_first + c) * ChunkShape<S>::kElems;
-  return reinterpret_cast<char*>(params) + (first_elem - pl.lo) * sizeof(typename S::storage);
-}
+// The segments one launch covers. Their chunks and edge tiles are numbered consecutively:
+// segment s owns chunks [chunk_end[s-1], chunk_end[s]) and edge tiles [edge_end[s-1], edge_end[s]).
+template <int N>
+struct Plans {
+  uint32_t count;
+  uint64_t chunk_end[N];
+  uint64_t edge_end[N];
+  Plan p[N];
+};
 
 __device__ __forceinline__ void load_chunk(u32x4 (&d)[kU], const char* base, uint32_t lane) {
 #pragma unroll
@@ -251,8 +265,36 @@ __device__ __forceinline__ void store_chunk(char* base, const u32x4 (&d)[kU], ui
   for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
 }
 
-__device__ __forceinline__ uint64_t edge_tile(const Plan& pl, uint64_t j) {
-  return j < pl.head_nt ? pl.head_t0 + j : pl.tail_t0 + (j - pl.head_nt);
+// Calls body(vbase, base) for every full chunk of the launch, one wave per chunk, where
+// vbase is the chunk's global vector index and base its byte address. A wave's chunk
+// indices increase, so its segment cursor only moves forward.
+template <class S, int N, class Body>
+__device__ __forceinline__ void for_each_chunk(const Plans<N>& ps, Body body) {
+  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
+  const uint64_t total = ps.chunk_end[ps.count - 1];
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint32_t s = 0;
+  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + wave; c < total; c += n_waves) {
+    while (c >= ps.chunk_end[s]) ++s;
+    const Plan& pl = ps.p[s];
+    const uint64_t chunk = pl.c_first + (c - (s ? ps.chunk_end[s - 1] : 0));
+    char* base = pl.base + (chunk * ChunkShape<S>::kElems - pl.lo) * sizeof(typename S::storage);
+    body(chunk * ChunkShape<S>::kVecs, base);
+  }
+}
+
+// Calls body(plan, tile) for every edge tile of the launch, one lane per tile.
+template <int N, class Body>
+__device__ __forceinline__ void for_each_edge(const Plans<N>& ps, Body body) {
+  const uint64_t n_edge = ps.edge_end[ps.count - 1];
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
+  for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
+    uint32_t s = 0;
+    while (j >= ps.edge_end[s]) ++s;
+    const Plan& pl = ps.p[s];
+    const uint64_t lj = j - (s ? ps.edge_end[s - 1] : 0);
+    body(pl, lj < pl.head_nt ? pl.head_t0 + lj : pl.tail_t0 + (lj - pl.head_nt));
+  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -264,16 +306,11 @@ struct Probe {
   __device__ __forceinline__ float delta(uint32_t byte) const { return ((byte >> bit) & 1u) ? eps : -eps; }
 };
 
-template <class S, bool TWO>
-__global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* params, Plan pl, Gen gen, Probe a,
-                                                        Probe b) {
+template <class S, bool TWO, int N>
+__global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, Probe a, Probe b) {
   const uint32_t lane = threadIdx.x & 63u;
   const bool shared_group = a.group == b.group;
-  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
-  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
-       c += n_waves) {
-    const uint64_t vbase = (pl.c_first + c) * ChunkShape<S>::kVecs;
-    char* base = chunk_base<S>(params, pl, c);
+  for_each_chunk<S>(ps, [&](uint64_t vbase, char* base) {
     u32x4 d[kU];
     load_chunk(d, base, lane);
     uint32_t Wa[kU][S::kWords], Wb[kU][S::kWords];
@@ -301,20 +338,17 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(typename S::storage* pa
       d[u] = S::pack(v);
     }
     store_chunk(base, d, lane);
-  }
-  const uint64_t n_edge = pl.head_nt + pl.tail_nt;
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
-    const uint64_t t = edge_tile(pl, j);
+  });
+  for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     const uint4 ra = gen.block(t, a.group);
     const uint4 rb = TWO ? gen.block(t, b.group) : ra;
     const uint32_t xa[4] = {ra.x, ra.y, ra.z, ra.w}, xb[4] = {rb.x, rb.y, rb.z, rb.w};
-    tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) {
+    tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
       float dv = a.delta(word_byte(xa[e >> 2], e & 3));
       if (TWO) dv = dv + b.delta(word_byte(xb[e >> 2], e & 3));
       return v + dv;
     });
-  }
+  });
 }
 
 // ---------------------------------------------------------------------------------------
@@ -343,15 +377,12 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
   __syncthreads();
 }
 
-// acc[u][e] (+)= table value of group g for each element of the chunk; on_words(g, W) sees
-// the group's generator words.
-template <class S, bool FIRST, class OnWords>
+// acc[u][e] (+)= table value of group g for each element of the chunk.
+template <class S, bool FIRST>
 __device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
-                                          uint64_t vbase, uint32_t lane, uint32_t g, uint32_t g_first,
-                                          OnWords& on_words) {
+                                          uint64_t vbase, uint32_t lane, uint32_t g, uint32_t g_first) {
   uint32_t W[kU][S::kWords];
   chunk_words(gen, vbase, lane, g_first + g, W, S());
-  on_words(g, W);
   const float* tg = tab + 256u * g;
 #pragma unroll
   for (int u = 0; u < kU; ++u)
@@ -364,21 +395,20 @@ __device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const 
 
 // Sum of the tables of groups 0 .. n_groups-1 for the chunk: NG > 0 fixes the count at
 // compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
-template <class S, int NG, class OnWords>
+template <class S, int NG>
 __device__ __forceinline__ void chunk_sums(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
-                                           uint64_t vbase, uint32_t lane, uint32_t n_groups, uint32_t g_first,
-                                           OnWords& on_words) {
+                                           uint64_t vbase, uint32_t lane, uint32_t n_groups, uint32_t g_first) {
   if constexpr (NG > 0) {
-    add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first, on_words);
+    add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first);
 #pragma unroll
-    for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first, on_words);
+    for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first);
   } else {
     float comp[kU][S::kVecElems];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
       float part[kU][S::kVecElems];
-      add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first, on_words);
+      add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first);
       const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
-      for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first, on_words);
+      for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first);
 #pragma unroll
       for (int u = 0; u < kU; ++u)
 #pragma unroll
@@ -437,10 +467,9 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 // RESTORE: theta + eps_r z_r - lr * sum (the last probe's restore merged with the update):
 // t = fl(theta + delta_r), then t - fl(lr * sum). The restore probe's words are generated
 // after the group loop (reusing the loop's words would keep them live across it).
-template <class S, int NG, bool RESTORE>
-__global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* params, Plan pl, Gen gen,
-                                                       uint32_t k_base, uint32_t K, uint32_t n_groups, Coefs cf,
-                                                       float lr, Probe r) {
+template <class S, int NG, bool RESTORE, int N>
+__global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
+                                                       uint32_t n_groups, Coefs cf, float lr, Probe r) {
   // n_groups x 256 floats: static for a fixed group count (constant LDS offsets), else dynamic.
   extern __shared__ float tab_dyn[];
   __shared__ float tab_fix[NG > 0 ? NG * 256 : 1];
@@ -448,16 +477,11 @@ __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* par
   build_tables(tab, cf, k_base, K, n_groups);
   const uint32_t g_first = k_base / 8;
   const uint32_t lane = threadIdx.x & 63u;
-  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
-  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); c < pl.n_chunks;
-       c += n_waves) {
-    const uint64_t vbase = (pl.c_first + c) * ChunkShape<S>::kVecs;
-    char* base = chunk_base<S>(params, pl, c);
+  for_each_chunk<S>(ps, [&](uint64_t vbase, char* base) {
     u32x4 d[kU];
     load_chunk(d, base, lane);
     float acc[kU][S::kVecElems];
-    auto no_words = [](uint32_t, const uint32_t (&)[kU][S::kWords]) {};
-    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first, no_words);
+    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
     uint32_t Wr[kU][S::kWords];  // the restore probe's generator words
     if (RESTORE) chunk_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
@@ -472,20 +496,17 @@ __global__ __launch_bounds__(kBlock) void update_kernel(typename S::storage* par
       d[u] = S::pack(v);
     }
     store_chunk(base, d, lane);
-  }
-  const uint64_t n_edge = pl.head_nt + pl.tail_nt;
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
-    const uint64_t t = edge_tile(pl, j);
+  });
+  for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
     tile_sums(acc, tab, gen, t, n_groups, g_first);
     const uint4 rr = RESTORE ? gen.block(t, r.group) : make_uint4(0, 0, 0, 0);
     const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
-    tile_elementwise<S>(params, pl.lo, pl.hi, t, [&](int e, float v) {
+    tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
       if (RESTORE) v = v + r.delta(word_byte(xr[e >> 2], e & 3));
       return v - lr * acc[e];
     });
-  }
+  });
 }
 
 // ---------------------------------------------------------------------------------------
@@ -500,6 +521,8 @@ __global__ __launch_bounds__(kBlock) void gen_bits_kernel(uint8_t* out, uint64_t
 
 // ---------------------------------------------------------------------------------------
 // Host side.
+constexpr int kSegsPerLaunch = 64;  // segments per batched launch (kernel arguments, ~5.6 KiB)
+
 uint32_t cap_blocks() { return g_max_blocks ? g_max_blocks : kDefaultMaxBlocks; }
 
 uint32_t grid_for(uint64_t work_items, uint64_t per_block) {
@@ -509,12 +532,11 @@ uint32_t grid_for(uint64_t work_items, uint64_t per_block) {
   return static_cast<uint32_t>(g ? g : 1);
 }
 
-int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n, size_t* elem) {
+int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n) {
   if (dt != ZO_F32 && dt != ZO_BF16) return ZO_ERR_ARG;
-  *elem = dt == ZO_F32 ? 4 : 2;
   if (n == 0) return ZO_OK;
   if (params == nullptr) return ZO_ERR_NULL;
-  if (reinterpret_cast<uintptr_t>(params) % *elem != 0) return ZO_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(params) % (dt == ZO_F32 ? 4 : 2) != 0) return ZO_ERR_ARG;
   if (offset + n < offset || offset + n == 0) return ZO_ERR_ARG;  // reaches 2^64
   return ZO_OK;
 }
@@ -523,10 +545,12 @@ uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
 
 // Full chunks need the address of global element 0 (params shifted back by offset
 // elements) to be 16-byte aligned, so that every chunk vector is an aligned 16 bytes.
-Plan make_plan(const void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t chunk_elems) {
+Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t chunk_elems) {
   Plan pl{};
+  pl.base = static_cast<char*>(params);
   pl.lo = offset;
   pl.hi = offset + n;
+  if (n == 0) return pl;
   const uintptr_t base = reinterpret_cast<uintptr_t>(params) - static_cast<uintptr_t>(offset * elem);
   uint64_t head_end = pl.hi, tail_begin = pl.hi;
   if ((base & 15u) == 0) {
@@ -549,9 +573,19 @@ Plan make_plan(const void* params, uint64_t offset, uint64_t n, size_t elem, uin
   return pl;
 }
 
-uint32_t plan_grid(const Plan& pl) {
-  const uint32_t a = pl.n_chunks ? grid_for(pl.n_chunks, kWavesPerBlock) : 1;
-  const uint32_t b = grid_for(pl.head_nt + pl.tail_nt, kBlock);
+template <int N>
+void add_plan(Plans<N>& ps, const Plan& pl) {
+  const uint32_t s = ps.count++;
+  ps.p[s] = pl;
+  ps.chunk_end[s] = (s ? ps.chunk_end[s - 1] : 0) + pl.n_chunks;
+  ps.edge_end[s] = (s ? ps.edge_end[s - 1] : 0) + pl.head_nt + pl.tail_nt;
+}
+
+template <int N>
+uint32_t plans_grid(const Plans<N>& ps) {
+  const uint64_t chunks = ps.chunk_end[ps.count - 1], edges = ps.edge_end[ps.count - 1];
+  const uint32_t a = chunks ? grid_for(chunks, kWavesPerBlock) : 1;
+  const uint32_t b = grid_for(edges, kBlock);
   return a > b ? a : b;
 }
 
@@ -559,94 +593,175 @@ int launch_status() { return hipGetLastError() == hipSuccess ? ZO_OK : ZO_ERR_HI
 
 Probe make_probe(uint32_t k, float eps) { return Probe{k / 8, k % 8, eps}; }
 
-template <class S>
-void launch_perturb(void* params, uint64_t offset, uint64_t n, const Gen& gen, const Probe& a, const Probe* b,
-                    hipStream_t st) {
-  const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
-  auto* p = static_cast<typename S::storage*>(params);
-  if (b)
-    perturb_kernel<S, true><<<dim3(plan_grid(pl)), dim3(kBlock), 0, st>>>(p, pl, gen, a, *b);
-  else
-    perturb_kernel<S, false><<<dim3(plan_grid(pl)), dim3(kBlock), 0, st>>>(p, pl, gen, a, a);
-}
-
-template <class S, bool RESTORE>
-void launch_update_r(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k_base, uint32_t K,
-                     uint32_t n_groups, const Coefs& cf, float lr, const Probe& r, hipStream_t st) {
-  const Plan pl = make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems);
-  const dim3 grid(plan_grid(pl)), block(kBlock);
-  const bool fixed = n_groups == 1 || n_groups == 2 || n_groups == 4 || n_groups == 8;
-  const size_t lds = fixed ? 0 : static_cast<size_t>(n_groups) * 256 * sizeof(float);
-  auto* p = static_cast<typename S::storage*>(params);
-  switch (n_groups) {
-    case 1: update_kernel<S, 1, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
-    case 2: update_kernel<S, 2, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
-    case 4: update_kernel<S, 4, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
-    case 8: update_kernel<S, 8, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
-    default: update_kernel<S, 0, RESTORE><<<grid, block, lds, st>>>(p, pl, gen, k_base, K, n_groups, cf, lr, r); break;
-  }
-}
-
-template <class S>
-void launch_update(void* params, uint64_t offset, uint64_t n, const Gen& gen, uint32_t k_base, uint32_t K,
-                   uint32_t n_groups, const Coefs& cf, float lr, const Probe* r, hipStream_t st) {
-  if (r)
-    launch_update_r<S, true>(params, offset, n, gen, k_base, K, n_groups, cf, lr, *r, st);
-  else
-    launch_update_r<S, false>(params, offset, n, gen, k_base, K, n_groups, cf, lr, Probe{0, 0, 0.0f}, st);
-}
-
 Gen make_gen(uint64_t seed, uint32_t step) {
   return Gen{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), step};
 }
 
-}  // namespace
+// What one sweep applies: one or two probes, or the update (with an optional restore probe).
+struct Sweep {
+  bool update;
+  Probe a, b;
+  bool two;
+  uint32_t k_base, K, n_groups;
+  Coefs cf;
+  float lr;
+  Probe r;
+  bool restore;
+};
 
-namespace {
-
-int perturb_impl(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
-                 const Probe& a, const Probe* b, void* stream) {
-  size_t elem = 0;
-  const int rc = check_params(params, dtype, offset, n, &elem);
-  if (rc != ZO_OK) return rc;
-  if (!std::isfinite(a.eps) || (b && !std::isfinite(b->eps))) return ZO_ERR_NONFINITE;
-  if (n == 0) return ZO_OK;
-  const Gen gen = make_gen(seed, step);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();
-  if (dtype == ZO_F32)
-    launch_perturb<F32>(params, offset, n, gen, a, b, st);
-  else
-    launch_perturb<BF16>(params, offset, n, gen, a, b, st);
-  return launch_status();
+template <class S, int N>
+void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, hipStream_t st) {
+  const dim3 grid(plans_grid(ps)), block(kBlock);
+  if (!w.update) {
+    if (w.two)
+      perturb_kernel<S, true, N><<<grid, block, 0, st>>>(ps, gen, w.a, w.b);
+    else
+      perturb_kernel<S, false, N><<<grid, block, 0, st>>>(ps, gen, w.a, w.a);
+    return;
+  }
+  const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
+  const size_t lds = fixed ? 0 : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
+  auto go = [&](auto kernel) {
+    if (lds > 65536)  // tables above 64 KiB: allow the workgroup the LDS it needs (<= 160 KiB)
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(lds));
+    kernel<<<grid, block, lds, st>>>(ps, gen, w.k_base, w.K, w.n_groups, w.cf, w.lr, w.r);
+  };
+  if (w.restore) {
+    switch (w.n_groups) {
+      case 1: go(update_kernel<S, 1, true, N>); break;
+      case 2: go(update_kernel<S, 2, true, N>); break;
+      case 4: go(update_kernel<S, 4, true, N>); break;
+      case 8: go(update_kernel<S, 8, true, N>); break;
+      default: go(update_kernel<S, 0, true, N>); break;
+    }
+  } else {
+    switch (w.n_groups) {
+      case 1: go(update_kernel<S, 1, false, N>); break;
+      case 2: go(update_kernel<S, 2, false, N>); break;
+      case 4: go(update_kernel<S, 4, false, N>); break;
+      case 8: go(update_kernel<S, 8, false, N>); break;
+      default: go(update_kernel<S, 0, false, N>); break;
+    }
+  }
 }
 
-int update_impl(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
-                uint32_t k_base, uint32_t K, const float* c, float lr, const Probe* r, void* stream) {
-  size_t elem = 0;
-  const int rc = check_params(params, dtype, offset, n, &elem);
-  if (rc != ZO_OK) return rc;
+int check_sweep(const Sweep& w) {
+  if (!std::isfinite(w.a.eps) || (w.two && !std::isfinite(w.b.eps))) return ZO_ERR_NONFINITE;
+  if (w.update && (!std::isfinite(w.lr) || (w.restore && !std::isfinite(w.r.eps)))) return ZO_ERR_NONFINITE;
+  return ZO_OK;
+}
+
+int make_update_sweep(Sweep& w, uint32_t k_base, uint32_t K, const float* c, float lr, const Probe* r) {
   if (K > ZO_K_MAX) return ZO_ERR_ARG;
   if (static_cast<uint64_t>(k_base) + K > (1ull << 32)) return ZO_ERR_ARG;
   if (K > 0 && c == nullptr) return ZO_ERR_NULL;
   if (!std::isfinite(lr) || (r && !std::isfinite(r->eps))) return ZO_ERR_NONFINITE;
   for (uint32_t j = 0; j < K; ++j)
     if (!std::isfinite(c[j])) return ZO_ERR_NONFINITE;
-  if (n == 0) return ZO_OK;
-  if (K == 0) return r ? perturb_impl(params, dtype, offset, n, seed, step, *r, nullptr, stream) : ZO_OK;
-  Coefs cf;
-  for (uint32_t j = 0; j < ZO_K_MAX; ++j) cf.c[j] = j < K ? c[j] : 0.0f;
+  w = Sweep{};
+  if (K == 0) {  // nothing to sum: the restore alone, or nothing
+    w.update = false;
+    w.a = r ? *r : Probe{0, 0, 0.0f};
+    return ZO_OK;
+  }
+  w.update = true;
+  for (uint32_t j = 0; j < ZO_K_MAX; ++j) w.cf.c[j] = j < K ? c[j] : 0.0f;
+  w.k_base = k_base;
+  w.K = K;
   const uint32_t g_first = k_base / 8;
   const uint32_t g_last = static_cast<uint32_t>((static_cast<uint64_t>(k_base) + K - 1) / 8);
-  const uint32_t n_groups = g_last - g_first + 1;
+  w.n_groups = g_last - g_first + 1;
+  w.lr = lr;
+  w.restore = r != nullptr && r->eps != 0.0f;  // a zero restore changes nothing (theta + 0 = theta)
+  w.r = r ? *r : Probe{0, 0, 0.0f};
+  return ZO_OK;
+}
+
+// One contiguous tensor.
+template <class S>
+int run_one(void* params, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step, const Sweep& w, void* stream) {
+  Plans<1> ps{};
+  add_plan(ps, make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems));
+  (void)hipGetLastError();
+  launch_sweep<S>(ps, make_gen(seed, step), w, static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int run_one_dt(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
+               const Sweep& w, void* stream) {
+  const int rc = check_params(params, dtype, offset, n);
+  if (rc != ZO_OK) return rc;
+  const int rs = check_sweep(w);
+  if (rs != ZO_OK) return rs;
+  if (n == 0) return ZO_OK;
+  return dtype == ZO_F32 ? run_one<F32>(params, offset, n, seed, step, w, stream)
+                         : run_one<BF16>(params, offset, n, seed, step, w, stream);
+}
+
+// A list of tensors: validated as a whole (alignment, index ranges, no two segments sharing
+// memory), then swept in launches of up to kSegsPerLaunch segments.
+int check_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype) {
+  if (dtype != ZO_F32 && dtype != ZO_BF16) return ZO_ERR_ARG;
+  if (n_segs == 0) return ZO_OK;
+  if (segs == nullptr) return ZO_ERR_NULL;
+  const size_t elem = dtype == ZO_F32 ? 4 : 2;
+  std::vector<std::pair<uintptr_t, uintptr_t>> spans;
+  spans.reserve(n_segs);
+  for (uint32_t i = 0; i < n_segs; ++i) {
+    const int rc = check_params(segs[i].params, dtype, segs[i].offset, segs[i].n);
+    if (rc != ZO_OK) return rc;
+    if (segs[i].n == 0) continue;
+    const uintptr_t a = reinterpret_cast<uintptr_t>(segs[i].params);
+    if (segs[i].n > (UINTPTR_MAX - a) / elem) return ZO_ERR_ARG;
+    spans.emplace_back(a, a + segs[i].n * elem);
+  }
+  std::sort(spans.begin(), spans.end());
+  for (size_t i = 1; i < spans.size(); ++i)
+    if (spans[i].first < spans[i - 1].second) return ZO_ERR_ARG;  // overlapping memory
+  return ZO_OK;
+}
+
+template <class S>
+int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_t step, const Sweep& w,
+                 void* stream) {
   const Gen gen = make_gen(seed, step);
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  if (dtype == ZO_F32)
-    launch_update<F32>(params, offset, n, gen, k_base, K, n_groups, cf, lr, r, st);
-  else
-    launch_update<BF16>(params, offset, n, gen, k_base, K, n_groups, cf, lr, r, st);
-  return launch_status();
+  Plans<kSegsPerLaunch> ps{};
+  for (uint32_t i = 0; i < n_segs; ++i) {
+    if (segs[i].n == 0) continue;
+    add_plan(ps, make_plan(segs[i].params, segs[i].offset, segs[i].n, sizeof(typename S::storage),
+                           ChunkShape<S>::kElems));
+    if (ps.count == kSegsPerLaunch) {
+      launch_sweep<S>(ps, gen, w, st);
+      if (launch_status() != ZO_OK) return ZO_ERR_HIP;
+      ps.count = 0;
+    }
+  }
+  if (ps.count) {
+    launch_sweep<S>(ps, gen, w, st);
+    return launch_status();
+  }
+  return ZO_OK;
+}
+
+int run_segments_dt(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed, uint32_t step,
+                    const Sweep& w, void* stream) {
+  const int rc = check_segments(segs, n_segs, dtype);
+  if (rc != ZO_OK) return rc;
+  const int rs = check_sweep(w);
+  if (rs != ZO_OK) return rs;
+  return dtype == ZO_F32 ? run_segments<F32>(segs, n_segs, seed, step, w, stream)
+                         : run_segments<BF16>(segs, n_segs, seed, step, w, stream);
+}
+
+Sweep perturb_sweep(uint32_t k_a, float eps_a, const uint32_t* k_b, float eps_b) {
+  Sweep w{};
+  w.a = make_probe(k_a, eps_a);
+  w.two = k_b != nullptr;
+  w.b = k_b ? make_probe(*k_b, eps_b) : w.a;
+  return w;
 }
 
 }  // namespace
@@ -655,30 +770,60 @@ extern "C" {
 
 int zo_perturb(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
                uint32_t k, float eps, void* stream) {
-  return perturb_impl(params, dtype, offset, n, seed, step, make_probe(k, eps), nullptr, stream);
+  return run_one_dt(params, dtype, offset, n, seed, step, perturb_sweep(k, eps, nullptr, 0.0f), stream);
 }
 
 int zo_perturb2(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
                 uint32_t k_a, float eps_a, uint32_t k_b, float eps_b, void* stream) {
-  const Probe b = make_probe(k_b, eps_b);
-  return perturb_impl(params, dtype, offset, n, seed, step, make_probe(k_a, eps_a), &b, stream);
+  return run_one_dt(params, dtype, offset, n, seed, step, perturb_sweep(k_a, eps_a, &k_b, eps_b), stream);
 }
 
 int zo_update_ex(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
                  uint32_t k_base, uint32_t K, const float* c, float lr, void* stream) {
-  return update_impl(params, dtype, offset, n, seed, step, k_base, K, c, lr, nullptr, stream);
+  const int rc = check_params(params, dtype, offset, n);
+  if (rc != ZO_OK) return rc;
+  Sweep w;
+  const int rs = make_update_sweep(w, k_base, K, c, lr, nullptr);
+  if (rs != ZO_OK) return rs;
+  if (!w.update || n == 0) return ZO_OK;
+  return run_one_dt(params, dtype, offset, n, seed, step, w, stream);
 }
 
 int zo_update(void* params, zo_dtype dtype, uint64_t n, uint64_t seed, uint32_t step, uint32_t K,
               const float* c, float lr, void* stream) {
-  return update_impl(params, dtype, 0, n, seed, step, 0, K, c, lr, nullptr, stream);
+  return zo_update_ex(params, dtype, 0, n, seed, step, 0, K, c, lr, stream);
 }
 
 int zo_update_restore(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
                       uint32_t k_base, uint32_t K, const float* c, float lr, uint32_t k_restore,
                       float eps_restore, void* stream) {
+  const int rc = check_params(params, dtype, offset, n);
+  if (rc != ZO_OK) return rc;
   const Probe r = make_probe(k_restore, eps_restore);
-  return update_impl(params, dtype, offset, n, seed, step, k_base, K, c, lr, &r, stream);
+  Sweep w;
+  const int rs = make_update_sweep(w, k_base, K, c, lr, &r);
+  if (rs != ZO_OK) return rs;
+  if (n == 0 || (!w.update && eps_restore == 0.0f)) return ZO_OK;
+  return run_one_dt(params, dtype, offset, n, seed, step, w, stream);
+}
+
+int zo_perturb_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed, uint32_t step,
+                        uint32_t k_a, float eps_a, uint32_t k_b, float eps_b, void* stream) {
+  const Sweep w = eps_b == 0.0f ? perturb_sweep(k_a, eps_a, nullptr, 0.0f) : perturb_sweep(k_a, eps_a, &k_b, eps_b);
+  return run_segments_dt(segs, n_segs, dtype, seed, step, w, stream);
+}
+
+int zo_update_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed, uint32_t step,
+                       uint32_t k_base, uint32_t K, const float* c, float lr, uint32_t k_restore,
+                       float eps_restore, void* stream) {
+  const int rc = check_segments(segs, n_segs, dtype);
+  if (rc != ZO_OK) return rc;
+  const Probe r = make_probe(k_restore, eps_restore);
+  Sweep w;
+  const int rs = make_update_sweep(w, k_base, K, c, lr, &r);
+  if (rs != ZO_OK) return rs;
+  if (!w.update && eps_restore == 0.0f) return ZO_OK;
+  return run_segments_dt(segs, n_segs, dtype, seed, step, w, stream);
 }
 
 int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_t seed, uint32_t step,

@@ -132,6 +132,35 @@ def test_sweep_validation_returns_before_launch(lib):
     assert lib.zo_gen_bits(None, 0, 0, 0, 0, 0, None) == zo.ZO_OK
 
 
+def test_segments_validation_returns_before_launch(lib):
+    Seg = zo.ZoSegment
+    c1 = (ctypes.c_float * 1)(1.0)
+
+    def arr(*segs):
+        a = (Seg * len(segs))()
+        for i, sg in enumerate(segs):
+            a[i] = Seg(*sg)
+        return a
+    ok = arr((0x10000, 0, 100), (0x20000, 100, 50))
+    assert lib.zo_perturb_segments(None, 3, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_NULL
+    assert lib.zo_perturb_segments(ok, 2, 9, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
+    assert lib.zo_perturb_segments(arr((None, 0, 5)), 1, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_NULL
+    assert lib.zo_perturb_segments(arr((0x10002, 0, 5)), 1, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
+    assert lib.zo_perturb_segments(arr((0x10000, 2 ** 64 - 2, 5)), 1, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
+    # overlapping memory (the second starts inside the first)
+    overl = arr((0x10000, 0, 100), (0x10000 + 4 * 99, 100, 10))
+    assert lib.zo_perturb_segments(overl, 2, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
+    overl_bf16 = arr((0x10000, 0, 100), (0x10000 + 2 * 50, 100, 10))
+    assert lib.zo_update_segments(overl_bf16, 2, zo.ZO_BF16, 0, 0, 0, 1, c1, 1e-3, 0, 0.0, None) == zo.ZO_ERR_ARG
+    assert lib.zo_perturb_segments(ok, 2, zo.ZO_F32, 0, 0, 0, float("nan"), 1, 1e-3, None) == zo.ZO_ERR_NONFINITE
+    big = (ctypes.c_float * (zo.ZO_K_MAX + 1))()
+    assert lib.zo_update_segments(ok, 2, zo.ZO_F32, 0, 0, 0, zo.ZO_K_MAX + 1, big, 1e-3, 0, 0.0, None) == zo.ZO_ERR_ARG
+    assert lib.zo_update_segments(ok, 2, zo.ZO_F32, 0, 0, 0, 1, c1, float("inf"), 0, 0.0, None) == zo.ZO_ERR_NONFINITE
+    # empty lists and empty segments are no-ops
+    assert lib.zo_perturb_segments(None, 0, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_OK
+    assert lib.zo_update_segments(arr((None, 0, 0)), 1, zo.ZO_F32, 0, 0, 0, 0, None, 1e-3, 0, 0.0, None) == zo.ZO_OK
+
+
 def test_strerror_and_version(lib):
     for s in (0, -1, -2, -3, -4, 99):
         assert lib.zo_strerror(s)

@@ -170,6 +170,7 @@ UPDATE_CASES = [
     (1000, 0, 0, 1), (4096, 0, 0, 4), (4097, 0, 0, 8), (3333, 5, 0, 9), (70_001, 0, 0, 16),
     (20_000, 2 ** 33 + 1, 0, 24), (20_000, 0, 0, 32), (50_000, 0, 0, 64), (9_000, 0, 0, 65),
     (5_000, 0, 0, 200), (3_000, 0, 0, 256), (10_000, 48, 3, 16), (10_000, 0, 8, 16), (7_000, 0, 100, 57),
+    (4_100, 0, 0, 512), (3_000, 17, 0, 1024), (2_500, 0, 5, 1024),
 ]
 
 
@@ -354,6 +355,88 @@ def test_full_tiny_step_fused():
     want, co, _ = oracle.full_step_fused(th, "f32", 0, 0, 0, w.eps, w.lr, lp, lm, l0)
     np.testing.assert_array_equal(c, co["c"])
     assert_f32_update_close(t.cpu().numpy(), want, c, w.lr)
+
+
+# ----------------------------------------------------------------------------- separate tensors
+def _model_tensors(dtype, sizes, seed):
+    """Separate device tensors (one allocation each) plus their global offsets in a flat layout."""
+    offs, o, ts, host = [], 0, [], []
+    for i, sz in enumerate(sizes):
+        h = workloads.normal_f32(sz, seed + i) if dtype == "f32" else workloads.normal_bf16_bits(sz, seed + i)
+        host.append(h)
+        ts.append(to_dev_f32(h) if dtype == "f32" else to_dev_bf16(h))
+        offs.append(o)
+        o += sz
+    return ts, offs, host
+
+
+SEG_SIZES = [5120 * 3 + 7, 5120, 5120, 16, 1, 0, 3000, 20_480 * 5, 5120, 2048, 4096 + 3]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_segments_match_flat_and_oracle(dtype):
+    """Each tensor of a segment list gets exactly what the oracle (and the flat call) gives it."""
+    ts, offs, host = _model_tensors(dtype, SEG_SIZES, 10)
+    seed, step, eps = 5, 2, 1e-3
+    c = np.random.default_rng(3).standard_normal(16).astype(np.float32)
+    get = (lambda t: t.cpu().numpy()) if dtype == "f32" else host_bits
+    zo.zo_perturb_segments(ts, offs, 3, eps, 0, 0.0, seed, step)
+    for t, o, h in zip(ts, offs, host):
+        np.testing.assert_array_equal(get(t), oracle.perturb(h, dtype, o, seed, step, 3, eps))
+    mid = [get(t) for t in ts]
+    zo.zo_perturb_segments(ts, offs, 3, eps, 4, eps, seed, step)
+    for t, o, m in zip(ts, offs, mid):
+        np.testing.assert_array_equal(get(t), oracle.perturb2(m, dtype, o, seed, step, 3, eps, 4, eps))
+    mid = [get(t) for t in ts]
+    # flat reference: the same values in one buffer, swept by the single-tensor call
+    flat_h = np.concatenate(mid)
+    flat = to_dev_f32(flat_h) if dtype == "f32" else to_dev_bf16(flat_h)
+    zo.zo_update_restore(flat, c, 1e-3, seed, step, 4, eps)
+    zo.zo_update_segments(ts, offs, c, 1e-3, seed, step, k_restore=4, eps_restore=eps)
+    flat_out = get(flat)
+    for t, o, m in zip(ts, offs, mid):
+        got = get(t)
+        np.testing.assert_array_equal(got, flat_out[o:o + m.size])
+        assert_restore_update_close(got, oracle.update_restore(m, dtype, o, seed, step, c, 1e-3, 4, eps), m, c,
+                                    1e-3, eps, dtype)
+
+
+def test_segments_many_launches_and_unaligned_views():
+    """150 tensors (three batched launches), some of them views that start mid-vector, in a
+    shuffled global order."""
+    rng = np.random.default_rng(4)
+    sizes = [int(s) for s in rng.integers(1, 9000, 150)]
+    base = [workloads.normal_bf16_bits(s + 3, 100 + i) for i, s in enumerate(sizes)]
+    owners = [to_dev_bf16(b) for b in base]
+    shifts = [int(x) for x in rng.integers(0, 4, 150)]
+    ts = [own[sh:sh + s] for own, sh, s in zip(owners, shifts, sizes)]
+    order = rng.permutation(150)
+    offs, o = [0] * 150, 7
+    for i in order:
+        offs[i] = o
+        o += sizes[i] + int(rng.integers(0, 40))
+    before = [host_bits(t) for t in ts]
+    c = rng.standard_normal(24).astype(np.float32)
+    zo.zo_perturb_segments(ts, offs, 9, 1e-3, 0, 0.0, 8, 8)
+    zo.zo_update_segments(ts, offs, c, 1e-3, 8, 8)
+    for t, own, sh, s, o_, b, orig in zip(ts, owners, shifts, sizes, offs, before, base):
+        p = oracle.perturb(b, "bf16", o_, 8, 8, 9, 1e-3)
+        assert_bf16_within_1ulp(host_bits(t), oracle.update(p, "bf16", o_, 8, 8, c, 1e-3), p, c, 1e-3)
+        full = host_bits(own)  # memory outside the view is untouched
+        np.testing.assert_array_equal(full[:sh], orig[:sh])
+        np.testing.assert_array_equal(full[sh + s:], orig[sh + s:])
+
+
+def test_segments_equal_flat_bits_for_update():
+    """The update over separate tensors is bit-identical to the update of the same flat buffer."""
+    ts, offs, host = _model_tensors("bf16", SEG_SIZES, 30)
+    flat = to_dev_bf16(np.concatenate(host))
+    c = np.random.default_rng(5).standard_normal(64).astype(np.float32)
+    zo.zo_update_segments(ts, offs, c, 1e-3, 1, 1)
+    zo.zo_update(flat, c, 1e-3, 1, 1)
+    flat_out = host_bits(flat)
+    for t, o, h in zip(ts, offs, host):
+        np.testing.assert_array_equal(host_bits(t), flat_out[o:o + h.size])
 
 
 # ----------------------------------------------------------------------------- full step
