@@ -8,15 +8,15 @@
 // Nothing but theta touches HBM.
 //
 // Memory layout of a sweep. theta is streamed in chunks of 64 x kU contiguous 16-byte
-// vectors per wave: vector u of lane l is chunk vector 64u + l, so every load and store
-// instruction of a wave covers 1 KiB of contiguous memory (non-temporal: nothing is
-// reused). A tile therefore spans kLanesPerTile adjacent lanes (2 for bf16, 4 for fp32).
-// Those lanes split the tile blocks of the chunk between them (each lane runs Philox for
-// kU / kLanesPerTile tiles) and hand each other the 32-bit words they need with DPP lane
-// swaps: bf16 lane pairs swap two words per block pair, fp32 lane quads transpose a 4x4
-// word matrix in two butterfly stages. Head and tail elements that do not fill a chunk
-// (and everything, when the storage is not 16-byte aligned relative to the global index)
-// take an element-wise path, one tile per lane.
+// vectors per wave: each load and store instruction of a wave covers 1 KiB of contiguous
+// memory (non-temporal: nothing is reused). A tile spans 2 vectors (bf16) or 4 (fp32); the
+// lanes holding one tile are m and m + 32 (bf16) or m, m + 16, m + 32, m + 48 (fp32), so
+// that the gfx950 half-wave swaps v_permlane32_swap / v_permlane16_swap exchange the
+// generator words: each lane runs Philox for kU / kLanesPerTile of the chunk's tiles, then
+// bf16 lane pairs swap two words per pair of blocks (two instructions) and fp32 lane groups
+// transpose a 4x4 word matrix (four instructions). Head and tail elements that do not fill a
+// chunk (and everything, when the storage is not 16-byte aligned relative to the global
+// index) take an element-wise path, one tile per lane.
 //
 // zo_perturb_segments / zo_update_segments sweep a list of separate tensors: the host validates
 // the list, builds one plan per tensor and launches batches of up to 64 plans (kernel
@@ -94,14 +94,6 @@ __device__ __forceinline__ float table_at(const float* tab, uint32_t w, int e) {
   return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + off);
 }
 
-// Lane exchanges inside a quad (DPP quad_perm): swap with lane ^ 1, with lane ^ 2.
-__device__ __forceinline__ uint32_t swap_lane1(uint32_t v) {
-  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0xB1, 0xF, 0xF, false));
-}
-__device__ __forceinline__ uint32_t swap_lane2(uint32_t v) {
-  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x4E, 0xF, 0xF, false));
-}
-
 // ---------------------------------------------------------------------------------------
 // Storage formats.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -167,48 +159,59 @@ template <class S>
 struct ChunkShape {
   static constexpr uint64_t kVecs = 64ull * kU;                      // vectors per chunk
   static constexpr uint64_t kElems = kVecs * S::kVecElems;           // bf16 2048, fp32 1024
-  static constexpr uint64_t kTiles = kElems / kTile;                 // bf16 128, fp32 64
-  static constexpr int kOwn = kU / S::kLanesPerTile;                 // blocks a lane generates
 };
 
+// Chunk vector held by a lane (for every u, lane l holds chunk vector 64u + vec_of_lane(l)):
+// the lanes of one tile sit 32 (bf16) or 16 (fp32) lanes apart.
+template <class S>
+__device__ __forceinline__ uint32_t vec_of_lane(uint32_t lane) {
+  return S::kLanesPerTile == 2 ? 2 * (lane & 31u) + (lane >> 5) : 4 * (lane & 15u) + (lane >> 4);
+}
+
 // For chunk vector base vbase (a global vector index, multiple of 64 kU) and probe group g:
-// W[u][w] = the generator words this lane's vector u needs. Lanes 2m, 2m+1 (bf16) or
-// 4m .. 4m+3 (fp32) share the tiles T(u) = (vbase + 64u) / kLanesPerTile + m.
+// W[u][w] = the generator words this lane's vector u needs.
+// bf16: lanes m and m + 32 hold the two halves of tile T(u) = vbase/2 + 32u + m; lane m + 32q
+// generates tiles 2j + q, and one permlane32 swap per word pair hands each lane the half it
+// needs (x,y for the first half, z,w for the second).
 __device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
                                             uint32_t (&W)[kU][BF16::kWords], BF16) {
-  const uint32_t q = lane & 1u;
-  const uint64_t t0 = vbase / 2 + (lane >> 1);
+  const uint32_t q = lane >> 5, m = lane & 31u;
+  const uint64_t t0 = vbase / 2 + m;
 #pragma unroll
   for (int j = 0; j < kU / 2; ++j) {
-    // this lane generates tile u = 2j + q; it needs words 2q, 2q+1 of tiles 2j and 2j+1
     const uint4 r = gen.block(t0 + 32ull * (2 * j + q), group);
-    const uint32_t own0 = q ? r.z : r.x, own1 = q ? r.w : r.y;
-    const uint32_t got0 = swap_lane1(q ? r.x : r.z), got1 = swap_lane1(q ? r.y : r.w);
-    W[2 * j][0] = q ? got0 : own0;
-    W[2 * j][1] = q ? got1 : own1;
-    W[2 * j + 1][0] = q ? own0 : got0;
-    W[2 * j + 1][1] = q ? own1 : got1;
+    const auto sx = __builtin_amdgcn_permlane32_swap(r.x, r.z, false, false);
+    const auto sy = __builtin_amdgcn_permlane32_swap(r.y, r.w, false, false);
+    W[2 * j][0] = sx[0];
+    W[2 * j][1] = sy[0];
+    W[2 * j + 1][0] = sx[1];
+    W[2 * j + 1][1] = sy[1];
   }
 }
 
+// fp32: lanes m + 16q (q = 0..3) hold the four quarters of tile T(u) = vbase/4 + 16u + m;
+// lane m + 16q generates tile T(q), and a 4x4 transpose across the four lanes (permlane32
+// swaps exchange the off-diagonal 2x2 blocks, permlane16 swaps the elements inside them)
+// leaves word q of tile T(u) in register u.
 __device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
                                             uint32_t (&W)[kU][F32::kWords], F32) {
-  // lane q of the quad generates tile T(q); after a 4x4 transpose across the quad, register
-  // u of lane q holds word q of tile T(u).
-  const uint32_t q = lane & 3u;
-  const uint4 r = gen.block(vbase / 4 + 16ull * q + (lane >> 2), group);
+  const uint32_t q = lane >> 4, m = lane & 15u;
+  const uint4 r = gen.block(vbase / 4 + 16ull * q + m, group);
   uint32_t a[4] = {r.x, r.y, r.z, r.w};
-  const bool hi1 = q & 1u, hi2 = q & 2u;
-#pragma unroll
-  for (int r0 = 0; r0 < 4; r0 += 2) {  // exchange off-diagonal elements of each 2x2 block
-    const uint32_t got = swap_lane1(hi1 ? a[r0] : a[r0 + 1]);
-    if (hi1) a[r0] = got; else a[r0 + 1] = got;
-  }
-#pragma unroll
-  for (int r0 = 0; r0 < 2; ++r0) {     // exchange off-diagonal 2x2 blocks
-    const uint32_t got = swap_lane2(hi2 ? a[r0] : a[r0 + 2]);
-    if (hi2) a[r0] = got; else a[r0 + 2] = got;
-  }
+  auto sw32 = [&](int i, int j) {
+    const auto p = __builtin_amdgcn_permlane32_swap(a[i], a[j], false, false);
+    a[i] = p[0];
+    a[j] = p[1];
+  };
+  auto sw16 = [&](int i, int j) {
+    const auto p = __builtin_amdgcn_permlane16_swap(a[i], a[j], false, false);
+    a[i] = p[0];
+    a[j] = p[1];
+  };
+  sw32(0, 2);
+  sw32(1, 3);
+  sw16(0, 1);
+  sw16(2, 3);
 #pragma unroll
   for (int u = 0; u < kU; ++u) W[u][0] = a[u];
 }
@@ -255,14 +258,18 @@ struct Plans {
   Plan p[N];
 };
 
+template <class S>
 __device__ __forceinline__ void load_chunk(u32x4 (&d)[kU], const char* base, uint32_t lane) {
+  const uint32_t v = vec_of_lane<S>(lane);
 #pragma unroll
-  for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + lane));
+  for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + v));
 }
 
+template <class S>
 __device__ __forceinline__ void store_chunk(char* base, const u32x4 (&d)[kU], uint32_t lane) {
+  const uint32_t v = vec_of_lane<S>(lane);
 #pragma unroll
-  for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + lane), d[u]);
+  for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + v), d[u]);
 }
 
 // Calls body(vbase, base) for every full chunk of the launch, one wave per chunk, where
@@ -312,7 +319,7 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
   const bool shared_group = a.group == b.group;
   for_each_chunk<S>(ps, [&](uint64_t vbase, char* base) {
     u32x4 d[kU];
-    load_chunk(d, base, lane);
+    load_chunk<S>(d, base, lane);
     uint32_t Wa[kU][S::kWords], Wb[kU][S::kWords];
     chunk_words(gen, vbase, lane, a.group, Wa, S());
     if (TWO) {
@@ -337,7 +344,7 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
       }
       d[u] = S::pack(v);
     }
-    store_chunk(base, d, lane);
+    store_chunk<S>(base, d, lane);
   });
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     const uint4 ra = gen.block(t, a.group);
@@ -479,7 +486,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
   const uint32_t lane = threadIdx.x & 63u;
   for_each_chunk<S>(ps, [&](uint64_t vbase, char* base) {
     u32x4 d[kU];
-    load_chunk(d, base, lane);
+    load_chunk<S>(d, base, lane);
     float acc[kU][S::kVecElems];
     chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
     uint32_t Wr[kU][S::kWords];  // the restore probe's generator words
@@ -495,7 +502,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
       }
       d[u] = S::pack(v);
     }
-    store_chunk(base, d, lane);
+    store_chunk<S>(base, d, lane);
   });
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
