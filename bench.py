@@ -55,7 +55,7 @@ def measured_counters(workload, K, dtype):
     return {}
 
 
-def cpu_baseline(w, K, budget_s=15.0):
+def cpu_baseline(w, K, budget_s=12.0):
     """The oracle on the host: one step (3K perturbs + one update) over a window of the workload."""
     import numpy as np
 
@@ -67,7 +67,7 @@ def cpu_baseline(w, K, budget_s=15.0):
     lp, lm, l0 = workloads.synthetic_losses(K, 0)
     windows, t_total, sweeps = 0, 0.0, 0
     rng = np.random.default_rng(1)
-    while t_total < budget_s and windows < 64:
+    while t_total < budget_s and windows < 1024:
         off = int(rng.integers(0, w.n - m))
         t0 = time.perf_counter()
         oracle.full_step(th, w.dtype, off, 2024, 0, w.eps, w.lr, lp, lm, l0)

@@ -51,9 +51,10 @@ def perturb(theta, dtype, offset, seed, step, k, eps, rounds=DEFAULT_ROUNDS):
     e = np.float32(eps)
     z = signs(offset, n, seed, step, k, rounds)
     delta = np.where(z > 0, e, -e).astype(np.float32)
-    if dtype == "f32":
-        return (theta + delta).astype(np.float32)
-    return f32_to_bf16(bf16_to_f32(theta) + delta)
+    with np.errstate(over="ignore", invalid="ignore"):  # IEEE: overflow gives inf, inf - inf NaN
+        if dtype == "f32":
+            return (theta + delta).astype(np.float32)
+        return f32_to_bf16(bf16_to_f32(theta) + delta)
 
 
 def perturb2(theta, dtype, offset, seed, step, k_a, eps_a, k_b, eps_b, rounds=DEFAULT_ROUNDS):
@@ -63,10 +64,11 @@ def perturb2(theta, dtype, offset, seed, step, k_a, eps_a, k_b, eps_b, rounds=DE
     ea, eb = np.float32(eps_a), np.float32(eps_b)
     da = np.where(signs(offset, n, seed, step, k_a, rounds) > 0, ea, -ea).astype(np.float32)
     db = np.where(signs(offset, n, seed, step, k_b, rounds) > 0, eb, -eb).astype(np.float32)
-    d = (da + db).astype(np.float32)
-    if dtype == "f32":
-        return (theta + d).astype(np.float32)
-    return f32_to_bf16(bf16_to_f32(theta) + d)
+    with np.errstate(over="ignore", invalid="ignore"):  # IEEE: overflow gives inf, inf - inf NaN
+        d = (da + db).astype(np.float32)
+        if dtype == "f32":
+            return (theta + d).astype(np.float32)
+        return f32_to_bf16(bf16_to_f32(theta) + d)
 
 
 def probe_sum(offset, n, seed, step, c, rounds=DEFAULT_ROUNDS, k_base=0):

@@ -151,6 +151,39 @@ def test_perturb_bf16_rounding_ties_and_subnormals():
         np.testing.assert_array_equal(host_bits(t), oracle.perturb(th, "bf16", 0, 77, 0, 3, eps))
 
 
+SPECIALS = [0.0, -0.0, np.inf, -np.inf, np.nan, 3.3895314e38, -3.3895314e38, 1e-40, -1e-40, 1.1754944e-38, 1.0]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("eps", [1e-3, 0.0, 3e38])
+def test_special_values_match_oracle(dtype, eps):
+    """Signed zeros, infinities, NaN, the largest finite values (overflow to inf), subnormals;
+    eps = 0 leaves finite weights unchanged. NaN is compared as NaN (its payload is not fixed)."""
+    n = 16 * 12 + 5
+    vals = np.array((SPECIALS * (n // len(SPECIALS) + 1))[:n], dtype=np.float32)
+    th = vals if dtype == "f32" else oracle.f32_to_bf16(vals)
+    t = to_dev_f32(th) if dtype == "f32" else to_dev_bf16(th)
+    zo.zo_perturb(t, 2, eps, 4, 4)
+    want = oracle.perturb(th, dtype, 0, 4, 4, 2, eps)
+    got = t.cpu().numpy() if dtype == "f32" else host_bits(t)
+    gf = got.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(got)
+    wf = want.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(want)
+    assert np.array_equal(np.isnan(gf), np.isnan(wf))
+    ok = ~np.isnan(wf)
+    np.testing.assert_array_equal(got[ok], want[ok])
+    c = np.array([0.5, -0.25], np.float32)
+    zo.zo_update(t, c, 1e-3, 4, 4)
+    u_want = oracle.update(want, dtype, 0, 4, 4, c, 1e-3)
+    u_got = t.cpu().numpy() if dtype == "f32" else host_bits(t)
+    uf = u_got.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(u_got)
+    wf = u_want.astype(np.float64) if dtype == "f32" else oracle.bf16_to_f64(u_want)
+    assert np.array_equal(np.isnan(uf), np.isnan(wf))
+    fin = np.isfinite(wf)
+    assert np.array_equal(uf[~fin & ~np.isnan(wf)], wf[~fin & ~np.isnan(wf)])  # infinities agree
+    err = np.abs(uf[fin] - wf[fin])
+    assert np.all(err <= 1e-6 * np.maximum(np.abs(wf[fin]), 1e-3 * 0.75) + (0 if dtype == "f32" else bf16_spacing(np.abs(wf[fin]))))
+
+
 def test_perturb_schedule_restores_fp32_within_1ulp():
     """Algorithm 1's +eps, -2 eps, +eps on the tiny workload: within 1 ulp of the largest intermediate."""
     th = workloads.tiny_theta()
