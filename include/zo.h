@@ -21,7 +21,7 @@
  *     retains it; it must stay valid until the stream work has finished.
  *   - offset: the global element index of params[0], so a shard or window of a larger
  *     parameter vector regenerates the same probe values as the whole vector would.
- *     offset + n must not exceed 2^64.
+ *     offset + n must be below 2^64.
  *   - stream: a hipStream_t (NULL = the default stream). Device work is enqueued on it
  *     and the call returns without waiting; faults surface at the caller's next
  *     synchronisation. Host arguments (coefficient arrays) are copied before return.
@@ -55,8 +55,8 @@ enum {
 #define ZO_K_MAX 1024u
 
 /* One tensor of a model's parameters, for the *_segments calls: `params` is caller-owned
- * device memory (aligned to the element size) holding n elements whose global element
- * indices are offset .. offset + n - 1. */
+ * device memory (aligned to the element size, on the device the stream belongs to) holding
+ * n elements whose global element indices are offset .. offset + n - 1. */
 typedef struct {
   void* params;
   uint64_t offset;

@@ -152,6 +152,9 @@ def _segments(tensors, offsets):
     dts = {t.dtype for t in tensors}
     if len(dts) > 1:
         raise TypeError("all tensors must share one dtype")
+    devs = {t.device for t in tensors}
+    if len(devs) > 1:
+        raise ValueError("all tensors must be on one device (the stream's)")
     arr = (ZoSegment * max(len(tensors), 1))()
     dt = ZO_F32
     for i, (t, o) in enumerate(zip(tensors, offsets)):

@@ -472,6 +472,28 @@ def test_segments_equal_flat_bits_for_update():
         np.testing.assert_array_equal(host_bits(t), flat_out[o:o + h.size])
 
 
+def test_concurrent_streams_on_disjoint_tensors():
+    """Calls on two streams over disjoint tensors run concurrently and give the serial results."""
+    a_h = workloads.normal_bf16_bits(3_000_017, 20)
+    b_h = workloads.normal_bf16_bits(2_000_003, 21)
+    a, b = to_dev_bf16(a_h), to_dev_bf16(b_h)
+    c = np.random.default_rng(6).standard_normal(16).astype(np.float32)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for it in range(3):
+        zo.zo_perturb(a, it, 1e-3, 1, 1, stream=s1)
+        zo.zo_perturb(b, it, -2e-3, 2, 1, stream=s2)
+    zo.zo_update(a, c, 1e-3, 1, 1, stream=s1)
+    zo.zo_update_ex(b, c[:8], 1e-3, 2, 1, offset=5, stream=s2)
+    torch.cuda.synchronize()
+    wa, wb = a_h, b_h
+    for it in range(3):
+        wa = oracle.perturb(wa, "bf16", 0, 1, 1, it, 1e-3)
+        wb = oracle.perturb(wb, "bf16", 0, 2, 1, it, -2e-3)
+    assert_bf16_within_1ulp(host_bits(a), oracle.update(wa, "bf16", 0, 1, 1, c, 1e-3), wa, c, 1e-3)
+    assert_bf16_within_1ulp(host_bits(b), oracle.update(wb, "bf16", 5, 2, 1, c[:8], 1e-3), wb, c[:8], 1e-3)
+
+
 # ----------------------------------------------------------------------------- full step
 def test_full_tiny_step():
     """The tiny fp32 workload: 2^20 weights, K = 4, eps 1e-3, lr 1e-4 (schedule + coeffs + update)."""
