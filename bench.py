@@ -31,6 +31,10 @@ METRIC = "fused probe-update effective HBM GB/s + params·probes/s (OPT-13B shap
 HBM_PEAK_GBPS = 8000.0
 # VALU issue peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a wave64 instruction takes 4 cycles).
 VALU_PEAK_TLANEOPS = 256 * 64 * 2.4e9 / 1e12
+# LDS: 128 bytes per clock per CU = 32 conflict-free 4-byte table reads per clock; uniform random
+# bytes into a 256-entry table on 32 banks cost 6.31 cycles per 64-lane read instead of 2.
+LDS_PEAK_GLOOKUPS = 256 * 32 * 2.4  # 1e9 lookups/s
+LDS_RANDOM_GLOOKUPS = 256 * 64 / 6.31 * 2.4
 
 
 def log(msg):
@@ -55,30 +59,51 @@ def measured_counters(workload, K, dtype):
     return {}
 
 
-def cpu_baseline(w, K, budget_s=12.0):
-    """The oracle on the host: one step (3K perturbs + one update) over a window of the workload."""
+_CPU = {}
+
+
+def _oracle_window(off):
+    """One full oracle step over the shared window at global offset `off` (a pool task)."""
+    import oracle
+    c = _CPU
+    oracle.full_step(c["theta"], c["dtype"], off, 2024, 0, c["eps"], c["lr"], c["lp"], c["lm"], c["l0"])
+    return 3 * c["K"] + 1
+
+
+def cpu_baseline(w, K, budget_s=12.0, procs=1):
+    """The oracle on the host: full steps (3K perturbs + one update) over windows of the
+    workload at random offsets, in one process or in `procs` forked worker processes that
+    each run whole windows. Must run before the GPU is touched (the workers are forked)."""
+    import multiprocessing
+
     import numpy as np
 
-    import oracle
     import workloads
 
     m = 1 << 16
-    th = workloads.normal_bf16_bits(m, 0)
     lp, lm, l0 = workloads.synthetic_losses(K, 0)
-    windows, t_total, sweeps = 0, 0.0, 0
+    _CPU.update(theta=workloads.normal_bf16_bits(m, 0) if w.dtype == "bf16" else workloads.normal_f32(m, 0),
+                dtype=w.dtype, eps=w.eps, lr=w.lr, lp=lp, lm=lm, l0=l0, K=K)
     rng = np.random.default_rng(1)
-    while t_total < budget_s and windows < 1024:
-        off = int(rng.integers(0, w.n - m))
-        t0 = time.perf_counter()
-        oracle.full_step(th, w.dtype, off, 2024, 0, w.eps, w.lr, lp, lm, l0)
-        t_total += time.perf_counter() - t0
-        windows += 1
-        sweeps += 3 * K + 1
+    offsets = [int(rng.integers(0, w.n - m)) for _ in range(1024)]
+    windows, sweeps = 0, 0
+    t0 = time.perf_counter()
+    if procs == 1:
+        while time.perf_counter() - t0 < budget_s and windows < len(offsets):
+            sweeps += _oracle_window(offsets[windows])
+            windows += 1
+    else:
+        with multiprocessing.get_context("fork").Pool(procs) as pool:
+            while time.perf_counter() - t0 < budget_s and windows + procs <= len(offsets):
+                sweeps += sum(pool.map(_oracle_window, offsets[windows:windows + procs], chunksize=1))
+                windows += procs
+    t_total = time.perf_counter() - t0
     b = 2 if w.dtype == "bf16" else 4
     gbps = sweeps * 2 * b * m / t_total / 1e9
-    return {"value": round(gbps, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    how = "single-threaded numpy" if procs == 1 else f"{procs} worker processes (one window each), numpy"
+    return {"value": round(gbps, 4), "unit": "GB/s", "cores": procs, "kind": "oracle",
             "sample": f"{windows} full steps (3K+1 = {3 * K + 1} sweeps) over windows of {m} weights at random "
-                      f"offsets of the {w.name} buffer, single-threaded numpy, {t_total:.1f} s; "
+                      f"offsets of the {w.name} buffer, {how}, {t_total:.1f} s wall; "
                       f"host {platform.processor() or platform.machine()}, os.cpu_count()={os.cpu_count()}"}
 
 
@@ -98,14 +123,22 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
-    import torch
-
-    import paper_2609_38095_amd as zo
     import workloads
 
     w = workloads.WORKLOADS[args.workload]
     K = args.K or w.K[0]
+    baselines = {}
+    if not args.no_cpu_baseline:
+        # before torch touches the GPU: the all-cores leg forks worker processes
+        log("timing the CPU oracle baseline (one process, then all cores)")
+        baselines["cpu_baseline"] = cpu_baseline(w, K)
+        baselines["cpu_baseline_all_cores"] = cpu_baseline(w, K, procs=min(16, os.cpu_count() or 1))
+
+    import numpy as np
+    import torch
+
+    import paper_2609_38095_amd as zo
+
     n, b = w.n, (2 if w.dtype == "bf16" else 4)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     dev = torch.device("cuda:0")
@@ -186,6 +219,34 @@ def main():
     fused_elapsed = time.perf_counter() - t0
     log(f"timed {args.steps} fused-schedule steps in {fused_elapsed:.3f} s")
 
+    # Plain in-place read-modify-write ceiling of this buffer (an even number of XOR passes
+    # leaves the weights as they were).
+    import ctypes
+    calib = ctypes.CDLL(os.path.join(os.path.dirname(zo.LIB_PATH), "libzo_calib.so"))
+    calib.zo_calib_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p]
+    sptr = ctypes.c_void_p(stream.cuda_stream)
+    buf_bytes = n * b - (n * b) % 16
+
+    def rmw():
+        rc = calib.zo_calib_rmw(ctypes.c_void_p(theta.data_ptr()), buf_bytes, 0x5A5A5A5A, sptr)
+        if rc != 0:
+            raise RuntimeError(f"zo_calib_rmw failed ({rc})")
+
+    rmw()
+    rmw()
+    ceil_ev = []
+    for _ in range(6):
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        rmw()
+        z.record(stream)
+        ceil_ev.append((a, z))
+    torch.cuda.synchronize()
+    ceil_ms = float(np.mean([a.elapsed_time(z) for a, z in ceil_ev]))
+    ceil_gbps = 2.0 * buf_bytes / (ceil_ms * 1e-3) / 1e9
+    log(f"plain read-modify-write ceiling of this buffer: {ceil_gbps:.1f} GB/s")
+
     ms = {k: np.array([a.elapsed_time(z) for a, z in v]) for k, v in ev.items()}
     t_step = elapsed / args.steps
     sweep_bytes = 2.0 * b * n
@@ -204,13 +265,26 @@ def main():
         r = {"kernel": kernel, "bound": "hbm", "achieved": round(gb, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
              "frac": round(hbm_frac, 4), "traffic": counters.get("traffic_bytes_per_launch", {}).get(kernel),
              "avg_ms": round(avg_ms, 4), "min_ms": round(float(d.min()), 4), "max_ms": round(float(d.max()), 4),
-             "launches": int(d.size), "bytes_per_launch": sweep_bytes, "hbm_frac": round(hbm_frac, 4)}
+             "launches": int(d.size), "bytes_per_launch": sweep_bytes, "hbm_frac": round(hbm_frac, 4),
+             "frac_of_rmw_ceiling": round(gb / ceil_gbps, 4)}
         if alu is not None:
             r["valu_tlaneops"] = round(alu, 2)
             r["alu_frac"] = round(alu / VALU_PEAK_TLANEOPS, 4)
-            if alu / VALU_PEAK_TLANEOPS > hbm_frac:
-                r.update(bound="alu", achieved=round(alu, 2), peak=round(VALU_PEAK_TLANEOPS, 2), unit="Tlane-op/s",
-                         frac=round(alu / VALU_PEAK_TLANEOPS, 4))
+        lds = counters.get("lds_per_launch", {}).get(kernel)
+        if kernel == "zo_update":
+            # one table lookup per element and probe group
+            glk = n * ((K + 7) // 8) / (avg_ms * 1e-3) / 1e9
+            r["table_glookups_per_s"] = round(glk, 1)
+            if lds is not None:
+                r["lds_busy"] = lds["lds_busy"]
+                if lds["lds_busy"] > max(hbm_frac, r.get("alu_frac", 0.0)):
+                    r.update(bound="lds", achieved=round(glk, 1), peak=round(LDS_PEAK_GLOOKUPS, 1),
+                             unit="G lookups/s", frac=round(glk / LDS_PEAK_GLOOKUPS, 4),
+                             peak_random_index=round(LDS_RANDOM_GLOOKUPS, 1),
+                             frac_of_random_index_peak=round(glk / LDS_RANDOM_GLOOKUPS, 4))
+        if alu is not None and r["bound"] == "hbm" and alu / VALU_PEAK_TLANEOPS > hbm_frac:
+            r.update(bound="alu", achieved=round(alu, 2), peak=round(VALU_PEAK_TLANEOPS, 2), unit="Tlane-op/s",
+                     frac=round(alu / VALU_PEAK_TLANEOPS, 4))
         return r
 
     out = {
@@ -235,6 +309,10 @@ def main():
         "step_params_probes_per_s": float(f"{n * 4 * K / t_step:.4e}"),
         "roofline": roof("zo_perturb", p_ms, p_gbps),
         "roofline_update": roof("zo_update", u_ms, u_gbps),
+        "rmw_ceiling": {"gbps": round(ceil_gbps, 1), "avg_ms": round(ceil_ms, 4), "launches": len(ceil_ev),
+                        "kernel": "plain in-place 16-byte XOR sweep of the same buffer (libzo_calib.so), "
+                                  "same memory shape as the sweeps, no probe work",
+                        "step_frac_of_ceiling": round(gbps / ceil_gbps, 4)},
         "fused_schedule": {
             "ms_per_step": round(fused_elapsed / args.steps * 1e3, 3),
             "sweeps_per_step": 2 * K + 1,
@@ -243,9 +321,7 @@ def main():
             "step_params_probes_per_s": float(f"{n * 4 * K / (fused_elapsed / args.steps):.4e}"),
         },
     }
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle baseline")
-        out["cpu_baseline"] = cpu_baseline(w, K)
+    out.update(baselines)
     print(json.dumps(out), flush=True)
 
 

@@ -1,4 +1,5 @@
-"""Compile libzo.so for gfx950 in-tree (hipcc for the HIP sweep, the host compiler for the rest)."""
+"""Compile libzo.so for gfx950 in-tree (hipcc for the HIP sweep, the host compiler for the rest),
+and libzo_calib.so, the read-modify-write ceiling probe the benchmark measures beside it."""
 
 import os
 import shutil
@@ -10,6 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libzo.so")
+CALIB_SRC = os.path.join(PKG, "calib", "rmw_ceiling.hip")
+CALIB_LIB = os.path.join(PKG, "libzo_calib.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -48,6 +51,9 @@ def build(verbose=False):
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB)
+    tmp = CALIB_LIB + ".tmp"
+    _run([HIPCC, *DEVICE_FLAGS, "-I", INCLUDE, "-shared", "-o", tmp, CALIB_SRC], verbose)
+    os.replace(tmp, CALIB_LIB)
     return LIB
 
 

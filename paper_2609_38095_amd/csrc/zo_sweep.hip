@@ -88,9 +88,16 @@ struct Gen {
 // Byte e (0..3) of a generator word: the probe byte of one element.
 __device__ __forceinline__ uint32_t word_byte(uint32_t w, int e) { return (w >> (8 * e)) & 0xFFu; }
 
-// Table entry selected by byte e of w, in a table of 256 floats (one SDWA shift for the address).
+// Table entry selected by byte e of w, in a table of 256 floats. The byte offset is one SDWA
+// shift for every byte (the compiler turns byte 0 into a shift and a mask unless told).
 __device__ __forceinline__ float table_at(const float* tab, uint32_t w, int e) {
-  const uint32_t off = ((w >> (8 * e)) & 0xFFu) << 2;
+  uint32_t off;
+  if (e == 0)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+        : "=v"(off)
+        : "v"(w));
+  else
+    off = ((w >> (8 * e)) & 0xFFu) << 2;
   return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + off);
 }
 
@@ -365,21 +372,26 @@ struct Coefs {
 };
 
 // Build the n_groups x 256 table in LDS. Entry (g, b): sum over the group's 8 probe slots
-// of +-c (bit set: +c); slots outside [k_base, k_base + K) contribute 0; pairwise.
+// of +-c (bit set: +c); slots outside [k_base, k_base + K) contribute 0; pairwise. Thread b
+// writes entry b of every group: the group loop and the coefficient reads are uniform (scalar
+// loads), and the sign of slot s is an XOR of the coefficient's sign bit with bit s of ~b.
+static_assert(kBlock == 256, "one table entry per thread");
 __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
                                              uint32_t n_groups) {
+  const uint32_t b = threadIdx.x;
+  uint32_t flip[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) flip[s] = ((~b) << (31 - s)) & 0x80000000u;
   const uint32_t g_first = k_base / 8;
-  for (uint32_t e = threadIdx.x; e < n_groups * 256u; e += kBlock) {
-    const uint32_t g = e >> 8, b = e & 255u;
+  for (uint32_t g = 0; g < n_groups; ++g) {
     float v[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const uint32_t k = 8u * (g_first + g) + s;
-      float cv = 0.0f;
-      if (k >= k_base && k - k_base < K) cv = cf.c[k - k_base];
-      v[s] = ((b >> s) & 1u) ? cv : -cv;
+      const float cv = (k >= k_base && k - k_base < K) ? cf.c[k - k_base] : 0.0f;
+      v[s] = __uint_as_float(__float_as_uint(cv) ^ flip[s]);
     }
-    tab[e] = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+    tab[256u * g + b] = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
   }
   __syncthreads();
 }

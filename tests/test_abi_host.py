@@ -24,8 +24,8 @@ def lib():
     return zo.library()
 
 
-def _declared_functions():
-    text = open(os.path.join(ROOT, "include", "zo.h")).read()
+def _declared_functions(header="zo.h"):
+    text = open(os.path.join(ROOT, "include", header)).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(zo_\w+)\s*\(", text)))
 
@@ -40,6 +40,21 @@ def test_library_exports_every_declared_symbol(lib):
     for name in _declared_functions():
         assert hasattr(lib, name), name
     assert set(zo.EXPORTS) == set(_declared_functions())
+
+
+def test_calibration_library_exports_its_header():
+    path = os.path.join(os.path.dirname(zo.LIB_PATH), "libzo_calib.so")
+    if not os.path.exists(path):
+        pytest.fail("libzo_calib.so is not built (run __graft_entry__.build())")
+    calib = ctypes.CDLL(path)
+    names = _declared_functions("zo_calib.h")
+    assert names == ["zo_calib_rmw"]
+    calib.zo_calib_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p]
+    # validation returns before any HIP call
+    assert calib.zo_calib_rmw(None, 0, 1, None) == 0
+    assert calib.zo_calib_rmw(None, 16, 1, None) == -1
+    assert calib.zo_calib_rmw(ctypes.c_void_p(0x1008), 16, 1, None) == -2
+    assert calib.zo_calib_rmw(ctypes.c_void_p(0x1000), 24, 1, None) == -2
 
 
 def test_header_constants_match_binding():
