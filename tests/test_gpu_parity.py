@@ -494,6 +494,46 @@ def test_concurrent_streams_on_disjoint_tensors():
     assert_bf16_within_1ulp(host_bits(b), oracle.update(wb, "bf16", 5, 2, 1, c[:8], 1e-3), wb, c[:8], 1e-3)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_graph_capture_replays_match_eager(dtype):
+    """A fused two-probe step captured into a HIP graph (through torch) and replayed three times,
+    with eager work and synchronisations between the replays, equals the same calls applied
+    eagerly the same number of times, bit for bit (the library records only kernel launches)."""
+    n = 300_007
+    if dtype == "f32":
+        h = workloads.normal_f32(n, 30)
+        a, g = torch.from_numpy(h).to(DEV), torch.from_numpy(h).to(DEV)
+    else:
+        h = workloads.normal_bf16_bits(n, 30)
+        a, g = to_dev_bf16(h), to_dev_bf16(h)
+    c = np.random.default_rng(8).standard_normal(2).astype(np.float32)
+    eps, lr, seed, step = 1e-3, 1e-3, 77, 4
+
+    def fused_step(t):
+        zo.zo_perturb(t, 0, eps, seed, step)
+        zo.zo_perturb(t, 0, -2 * eps, seed, step)
+        zo.zo_perturb2(t, 0, eps, 1, eps, seed, step)
+        zo.zo_perturb(t, 1, -2 * eps, seed, step)
+        zo.zo_update_restore(t, c, lr, seed, step, 1, eps)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        fused_step(g)
+    torch.cuda.synchronize()
+    bits = (lambda t: t.cpu().numpy().view(np.uint32)) if dtype == "f32" else host_bits
+    np.testing.assert_array_equal(bits(g), bits(a))  # capture launches nothing
+    scratch = torch.ones(1 << 16, device=DEV)
+    for replay in range(3):
+        fused_step(a)
+        graph.replay()
+        scratch.mul_(1.5)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(bits(g), bits(a), err_msg=f"replay {replay}")
+
+
 # ----------------------------------------------------------------------------- full step
 def test_full_tiny_step():
     """The tiny fp32 workload: 2^20 weights, K = 4, eps 1e-3, lr 1e-4 (schedule + coeffs + update)."""
@@ -513,7 +553,7 @@ def test_full_tiny_step():
 
 
 # ----------------------------------------------------------------------------- full size
-def _windows(n, rng, count=24, size=1 << 15, boundaries=()):
+def _windows(n, rng, count, size, boundaries=()):
     starts = [0, n - size, n - 37] + [int(b) - size // 2 for b in boundaries]
     starts += [int(s) for s in rng.integers(0, n - size, count)]
     return sorted({min(max(s, 0), n - 1) for s in starts})
@@ -521,8 +561,11 @@ def _windows(n, rng, count=24, size=1 << 15, boundaries=()):
 
 @pytest.mark.parametrize("name,K", [("opt125m", 16), ("opt13b", 16), ("opt1.3b", 64), ("opt30b", 32)])
 def test_full_size_sampled_windows(name, K):
-    """At the full OPT-shaped size, in the benchmark's launch configuration: one perturb and one
-    update checked on windows (first, last incl. the ragged tail, tensor boundaries, random)."""
+    """At the full OPT-shaped size, in the benchmark's launch configuration, on 32 random
+    windows of 2^20 weights plus the first window, the last (with the ragged tail) and windows
+    across tensor boundaries: one perturb and one two-probe transition checked bit for bit on
+    every window; the update and the update-with-restore checked on the first and last 2^15
+    weights of every window (the oracle's K-probe sums are the slow part)."""
     w = workloads.WORKLOADS[name]
     n = w.n
     note(f"full-size {name}: n {n} K {K}")
@@ -531,8 +574,9 @@ def test_full_size_sampled_windows(name, K):
     rng = np.random.default_rng(7)
     offs = [o for _, o, _ in workloads.tensor_offsets(w)]
     bounds = [offs[1], offs[2], offs[len(offs) // 2], offs[-2]]
-    size = 1 << 15
-    wins = _windows(n, rng, 24, size, bounds)
+    size, part = 1 << 20, 1 << 15
+    wins = _windows(n, rng, 32, size, bounds)
+    assert len(wins) >= 32
     grab = lambda: [host_bits(buf[s:min(s + size, n)]) for s in wins]
     seed, step = 2024, 3
     before = grab()
@@ -551,7 +595,13 @@ def test_full_size_sampled_windows(name, K):
     torch.cuda.empty_cache()
     for s, b, m, a, tr, f in zip(wins, before, mid, after, trans, final):
         np.testing.assert_array_equal(m, oracle.perturb(b, "bf16", s, seed, step, 5, w.eps))
-        assert_bf16_within_1ulp(a, oracle.update(m, "bf16", s, seed, step, c, w.lr), m, c, w.lr)
         np.testing.assert_array_equal(tr, oracle.perturb2(a, "bf16", s, seed, step, 5, w.eps, 6, w.eps))
-        assert_restore_update_close(f, oracle.update_restore(tr, "bf16", s, seed, step, c, w.lr, 6, w.eps),
-                                    tr, c, w.lr, w.eps, "bf16")
+        m_len = len(m)
+        for lo in sorted({0, max(m_len - part, 0)}):
+            hi = min(lo + part, m_len)
+            g = s + lo
+            assert_bf16_within_1ulp(a[lo:hi], oracle.update(m[lo:hi], "bf16", g, seed, step, c, w.lr),
+                                    m[lo:hi], c, w.lr)
+            assert_restore_update_close(f[lo:hi],
+                                        oracle.update_restore(tr[lo:hi], "bf16", g, seed, step, c, w.lr, 6, w.eps),
+                                        tr[lo:hi], c, w.lr, w.eps, "bf16")
