@@ -41,7 +41,7 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def measured_counters(workload, K, dtype):
+def measured_counters(workload, K, dtype, layout="flat"):
     """Per-launch HBM bytes (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known
     size) and VALU instruction counts (SQ_INSTS_VALU) from the committed rocprofv3 summaries,
     keyed by kernel; {} when none matches this workload or the sweep source has changed since
@@ -54,7 +54,8 @@ def measured_counters(workload, K, dtype):
         for line in open(path):
             if line.startswith("counters-json:"):
                 d = json.loads(line.split(":", 1)[1])
-                if (d.get("workload"), d.get("K"), d.get("dtype"), d.get("source_sha256")) == (workload, K, dtype, digest):
+                key = (d.get("workload"), d.get("K"), d.get("dtype"), d.get("layout", "flat"), d.get("source_sha256"))
+                if key == (workload, K, dtype, layout, digest):
                     return d
     return {}
 
@@ -114,6 +115,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="opt13b", help="tiny, opt125m, opt1.3b, opt13b or opt30b")
     ap.add_argument("--K", type=int, default=0, help="probes per step (default: the workload's first)")
+    ap.add_argument("--layout", default="flat", choices=["flat", "tensors"],
+                    help="flat: one contiguous buffer (zo_perturb, zo_update); tensors: every OPT tensor "
+                         "allocated separately, swept with zo_perturb_segments / zo_update_segments")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="before warmup, run one plain device copy of this many GiB (calibrates HBM byte counters)")
@@ -127,6 +131,9 @@ def main():
 
     w = workloads.WORKLOADS[args.workload]
     K = args.K or w.K[0]
+    if args.layout == "tensors" and not w.hidden:
+        print(f"--layout tensors needs an OPT-shaped workload ({w.name} is one flat vector)", file=sys.stderr)
+        sys.exit(2)
     baselines = {}
     if not args.no_cpu_baseline:
         # before torch touches the GPU: the all-cores leg forks worker processes
@@ -145,11 +152,33 @@ def main():
     zo.library()
     log(f"workload {w.name}: n={n} dtype={w.dtype} K={K} eps={w.eps} lr={w.lr}; {n * b / 1e9:.2f} GB of weights")
 
-    theta = torch.empty(n, dtype=dt, device=dev)
-    if w.hidden:
-        workloads.fill_opt_buffer_device(theta, w)
+    seed = 2024
+    stream = torch.cuda.current_stream(dev)
+    if args.layout == "flat":
+        theta = torch.empty(n, dtype=dt, device=dev)
+        if w.hidden:
+            workloads.fill_opt_buffer_device(theta, w)
+        else:
+            theta.copy_(torch.from_numpy(workloads.tiny_theta(n)))
+        n_tensors = 1
+        perturb = lambda k, e, step: zo.zo_perturb(theta, k, e, seed, step, stream=stream)
+        perturb2 = lambda ka, ea, kb, eb, step: zo.zo_perturb2(theta, ka, ea, kb, eb, seed, step, stream=stream)
+        update = lambda c, step: zo.zo_update(theta, c, w.lr, seed, step, stream=stream)
+        update_restore = lambda c, step, kr, er: zo.zo_update_restore(theta, c, w.lr, seed, step, kr, er,
+                                                                      stream=stream)
     else:
-        theta.copy_(torch.from_numpy(workloads.tiny_theta(n)))
+        spans = workloads.tensor_offsets(w)
+        tensors = [torch.empty(sz, dtype=dt, device=dev) for _, _, sz in spans]
+        offs = [o for _, o, _ in spans]
+        workloads.fill_opt_tensors_device(tensors, w)
+        n_tensors = len(tensors)
+        perturb = lambda k, e, step: zo.zo_perturb_segments(tensors, offs, k, e, 0, 0.0, seed, step, stream=stream)
+        perturb2 = lambda ka, ea, kb, eb, step: zo.zo_perturb_segments(tensors, offs, ka, ea, kb, eb, seed, step,
+                                                                       stream=stream)
+        update = lambda c, step: zo.zo_update_segments(tensors, offs, c, w.lr, seed, step, stream=stream)
+        update_restore = lambda c, step, kr, er: zo.zo_update_segments(tensors, offs, c, w.lr, seed, step, kr, er,
+                                                                       stream=stream)
+        log(f"per-tensor layout: {n_tensors} separately allocated tensors")
     torch.cuda.synchronize()
     if args.calib_copy_gib > 0:
         nb = int(args.calib_copy_gib * 2 ** 30)
@@ -161,8 +190,6 @@ def main():
         log(f"calibration copy: {nb} bytes read, {nb} bytes written")
         del src, dst
         torch.cuda.empty_cache()
-    stream = torch.cuda.current_stream(dev)
-    seed = 2024
 
     ev = {"perturb": [], "update": []}
 
@@ -179,24 +206,24 @@ def main():
         for k in range(K):
             for e in (w.eps, -2.0 * w.eps, w.eps):
                 if record:
-                    timed("perturb", lambda: zo.zo_perturb(theta, k, e, seed, step, stream=stream))
+                    timed("perturb", lambda: perturb(k, e, step))
                 else:
-                    zo.zo_perturb(theta, k, e, seed, step, stream=stream)
+                    perturb(k, e, step)
         c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
         if record:
-            timed("update", lambda: zo.zo_update(theta, c, w.lr, seed, step, stream=stream))
+            timed("update", lambda: update(c, step))
         else:
-            zo.zo_update(theta, c, w.lr, seed, step, stream=stream)
+            update(c, step)
 
     def fused_step(step):
         lp, lm, l0 = workloads.synthetic_losses(K, step)
-        zo.zo_perturb(theta, 0, w.eps, seed, step, stream=stream)
+        perturb(0, w.eps, step)
         for k in range(K):
-            zo.zo_perturb(theta, k, -2.0 * w.eps, seed, step, stream=stream)
+            perturb(k, -2.0 * w.eps, step)
             if k + 1 < K:
-                zo.zo_perturb2(theta, k, w.eps, k + 1, w.eps, seed, step, stream=stream)
+                perturb2(k, w.eps, k + 1, w.eps, step)
         c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
-        zo.zo_update_restore(theta, c, w.lr, seed, step, K - 1, w.eps, stream=stream)
+        update_restore(c, step, K - 1, w.eps)
 
     for s in range(args.warmup):
         one_step(s, False)
@@ -219,33 +246,37 @@ def main():
     fused_elapsed = time.perf_counter() - t0
     log(f"timed {args.steps} fused-schedule steps in {fused_elapsed:.3f} s")
 
-    # Plain in-place read-modify-write ceiling of this buffer (an even number of XOR passes
-    # leaves the weights as they were).
-    import ctypes
-    calib = ctypes.CDLL(os.path.join(os.path.dirname(zo.LIB_PATH), "libzo_calib.so"))
-    calib.zo_calib_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p]
-    sptr = ctypes.c_void_p(stream.cuda_stream)
-    buf_bytes = n * b - (n * b) % 16
+    # Plain in-place read-modify-write ceiling of the flat buffer (an even number of XOR passes
+    # leaves the weights as they were). Not measured for the per-tensor layout, where a plain
+    # sweep would need one launch per tensor.
+    ceil_gbps = ceil_ms = None
+    ceil_launches = 6
+    if args.layout == "flat":
+        import ctypes
+        calib = ctypes.CDLL(os.path.join(os.path.dirname(zo.LIB_PATH), "libzo_calib.so"))
+        calib.zo_calib_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p]
+        sptr = ctypes.c_void_p(stream.cuda_stream)
+        buf_bytes = n * b - (n * b) % 16
 
-    def rmw():
-        rc = calib.zo_calib_rmw(ctypes.c_void_p(theta.data_ptr()), buf_bytes, 0x5A5A5A5A, sptr)
-        if rc != 0:
-            raise RuntimeError(f"zo_calib_rmw failed ({rc})")
+        def rmw():
+            rc = calib.zo_calib_rmw(ctypes.c_void_p(theta.data_ptr()), buf_bytes, 0x5A5A5A5A, sptr)
+            if rc != 0:
+                raise RuntimeError(f"zo_calib_rmw failed ({rc})")
 
-    rmw()
-    rmw()
-    ceil_ev = []
-    for _ in range(6):
-        a = torch.cuda.Event(enable_timing=True)
-        z = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
         rmw()
-        z.record(stream)
-        ceil_ev.append((a, z))
-    torch.cuda.synchronize()
-    ceil_ms = float(np.mean([a.elapsed_time(z) for a, z in ceil_ev]))
-    ceil_gbps = 2.0 * buf_bytes / (ceil_ms * 1e-3) / 1e9
-    log(f"plain read-modify-write ceiling of this buffer: {ceil_gbps:.1f} GB/s")
+        rmw()
+        ceil_ev = []
+        for _ in range(ceil_launches):
+            a = torch.cuda.Event(enable_timing=True)
+            z = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            rmw()
+            z.record(stream)
+            ceil_ev.append((a, z))
+        torch.cuda.synchronize()
+        ceil_ms = float(np.mean([a.elapsed_time(z) for a, z in ceil_ev]))
+        ceil_gbps = 2.0 * buf_bytes / (ceil_ms * 1e-3) / 1e9
+        log(f"plain read-modify-write ceiling of this buffer: {ceil_gbps:.1f} GB/s")
 
     ms = {k: np.array([a.elapsed_time(z) for a, z in v]) for k, v in ev.items()}
     t_step = elapsed / args.steps
@@ -255,7 +286,7 @@ def main():
     p_ms, u_ms = float(ms["perturb"].mean()), float(ms["update"].mean())
     p_gbps, u_gbps = sweep_bytes / (p_ms * 1e-3) / 1e9, sweep_bytes / (u_ms * 1e-3) / 1e9
 
-    counters = measured_counters(w.name, K, w.dtype)
+    counters = measured_counters(w.name, K, w.dtype, args.layout)
 
     def roof(kernel, avg_ms, gb):
         d = ms["perturb" if kernel == "zo_perturb" else "update"]
@@ -266,7 +297,10 @@ def main():
              "frac": round(hbm_frac, 4), "traffic": counters.get("traffic_bytes_per_launch", {}).get(kernel),
              "avg_ms": round(avg_ms, 4), "min_ms": round(float(d.min()), 4), "max_ms": round(float(d.max()), 4),
              "launches": int(d.size), "bytes_per_launch": sweep_bytes, "hbm_frac": round(hbm_frac, 4),
-             "frac_of_rmw_ceiling": round(gb / ceil_gbps, 4)}
+             "frac_of_rmw_ceiling": round(gb / ceil_gbps, 4) if ceil_gbps else None}
+        if args.layout == "tensors":
+            r["per_sweep"] = (f"one call covers {n_tensors} tensors in {-(-n_tensors // 64)} launches; "
+                              "times are per call")
         if alu is not None:
             r["valu_tlaneops"] = round(alu, 2)
             r["alu_frac"] = round(alu / VALU_PEAK_TLANEOPS, 4)
@@ -300,7 +334,11 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic (seeded OPT-shaped weights ~N(0,0.02), losses ~N(2.0,0.05))",
-        "config": {"workload": f"{w.name}-shaped flat {w.dtype} parameter set, full 1.5-SPSA step",
+        "config": {"workload": (f"{w.name}-shaped flat {w.dtype} parameter set, full 1.5-SPSA step"
+                                if args.layout == "flat" else
+                                f"{w.name}-shaped {w.dtype} parameter set as {n_tensors} separately allocated "
+                                f"tensors, full 1.5-SPSA step"),
+                   "layout": args.layout, "n_tensors": n_tensors,
                    "n_params": n, "K": K, "eps": w.eps, "lr": w.lr, "sweeps_per_step": 3 * K + 1,
                    "parallelism": "single GPU"},
         "update_gbps": round(u_gbps, 1),
@@ -309,10 +347,11 @@ def main():
         "step_params_probes_per_s": float(f"{n * 4 * K / t_step:.4e}"),
         "roofline": roof("zo_perturb", p_ms, p_gbps),
         "roofline_update": roof("zo_update", u_ms, u_gbps),
-        "rmw_ceiling": {"gbps": round(ceil_gbps, 1), "avg_ms": round(ceil_ms, 4), "launches": len(ceil_ev),
-                        "kernel": "plain in-place 16-byte XOR sweep of the same buffer (libzo_calib.so), "
-                                  "same memory shape as the sweeps, no probe work",
-                        "step_frac_of_ceiling": round(gbps / ceil_gbps, 4)},
+        "rmw_ceiling": None if ceil_gbps is None else {
+            "gbps": round(ceil_gbps, 1), "avg_ms": round(ceil_ms, 4), "launches": ceil_launches,
+            "kernel": "plain in-place 16-byte XOR sweep of the same buffer (libzo_calib.so), "
+                      "same memory shape as the sweeps, no probe work",
+            "step_frac_of_ceiling": round(gbps / ceil_gbps, 4)},
         "fused_schedule": {
             "ms_per_step": round(fused_elapsed / args.steps * 1e3, 3),
             "sweeps_per_step": 2 * K + 1,

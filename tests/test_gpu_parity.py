@@ -605,3 +605,48 @@ def test_full_size_sampled_windows(name, K):
             assert_restore_update_close(f[lo:hi],
                                         oracle.update_restore(tr[lo:hi], "bf16", g, seed, step, c, w.lr, 6, w.eps),
                                         tr[lo:hi], c, w.lr, w.eps, "bf16")
+
+
+def test_full_size_separate_tensors():
+    """OPT-13B as 644 separately allocated tensors, in the benchmark's per-tensor launch
+    configuration (batches of 64 tensors per launch): a segmented perturb, two-probe transition,
+    update and update-with-restore, checked against the oracle with each tensor's global offset
+    on the first and last 2^15 weights of the first, last, largest and 24 random tensors."""
+    w = workloads.WORKLOADS["opt13b"]
+    spans = workloads.tensor_offsets(w)
+    note(f"full-size opt13b as {len(spans)} tensors")
+    tensors = [torch.empty(sz, dtype=torch.bfloat16, device=DEV) for _, _, sz in spans]
+    offs = [o for _, o, _ in spans]
+    workloads.fill_opt_tensors_device(tensors, w)
+    rng = np.random.default_rng(11)
+    pick = {0, len(spans) - 1, int(np.argmax([sz for _, _, sz in spans]))}
+    pick |= {int(i) for i in rng.integers(0, len(spans), 24)}
+    part = 1 << 15
+    wins = []  # (tensor index, local start, global start, length)
+    for i in sorted(pick):
+        sz = spans[i][2]
+        for lo in sorted({0, max(sz - part, 0)}):
+            wins.append((i, lo, offs[i] + lo, min(part, sz - lo)))
+    grab = lambda: [host_bits(tensors[i][lo:lo + m]) for i, lo, _, m in wins]
+    seed, step, K = 2024, 5, 16
+    lp, lm, l0 = workloads.synthetic_losses(K, step)
+    c = zo.zo_probe_coeffs(lp, lm, l0, w.eps)
+    before = grab()
+    zo.zo_perturb_segments(tensors, offs, 3, w.eps, 0, 0.0, seed, step)
+    mid = grab()
+    zo.zo_perturb_segments(tensors, offs, 3, -2 * w.eps, 4, w.eps, seed, step)
+    trans = grab()
+    zo.zo_update_segments(tensors, offs, c, w.lr, seed, step)
+    after = grab()
+    zo.zo_update_segments(tensors, offs, c, w.lr, seed, step, 4, -w.eps)
+    final = grab()
+    torch.cuda.synchronize()
+    del tensors
+    torch.cuda.empty_cache()
+    for (i, lo, g, m), b, md, tr, a, f in zip(wins, before, mid, trans, after, final):
+        np.testing.assert_array_equal(md, oracle.perturb(b, "bf16", g, seed, step, 3, w.eps), err_msg=f"tensor {i}")
+        np.testing.assert_array_equal(tr, oracle.perturb2(md, "bf16", g, seed, step, 3, -2 * w.eps, 4, w.eps),
+                                      err_msg=f"tensor {i}")
+        assert_bf16_within_1ulp(a, oracle.update(tr, "bf16", g, seed, step, c, w.lr), tr, c, w.lr)
+        assert_restore_update_close(f, oracle.update_restore(a, "bf16", g, seed, step, c, w.lr, 4, -w.eps),
+                                    a, c, w.lr, -w.eps, "bf16")

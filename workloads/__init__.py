@@ -95,24 +95,29 @@ def normal_bf16_bits(n, seed, scale=0.02):
     return x.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16).copy()
 
 
-def fill_opt_buffer_device(buf, w):
-    """Fill a flat device tensor (dtype matching w) with the OPT-shaped synthetic weights.
-
-    Each 'normal' tensor is drawn on the device from torch.Generator seeded 1000 + index.
-    """
+def fill_opt_tensors_device(tensors, w):
+    """Fill device tensors, one per OPT tensor in order (dtype matching w), with the OPT-shaped
+    synthetic weights: each 'normal' tensor is drawn on the device from torch.Generator seeded
+    1000 + index; biases and LayerNorm betas are 0 and gammas 1."""
     import torch
-    off = 0
-    for idx, (name, sz, kind) in enumerate(opt_tensors(w)):
-        view = buf[off:off + sz]
-        off += sz
+    for idx, ((name, sz, kind), t) in enumerate(zip(opt_tensors(w), tensors)):
+        if t.numel() != sz:
+            raise ValueError(f"tensor {idx} ({name}) holds {t.numel()} elements, expected {sz}")
         if kind == "zero":
-            view.zero_()
+            t.zero_()
         elif kind == "one":
-            view.fill_(1.0)
+            t.fill_(1.0)
         else:
-            g = torch.Generator(device=buf.device)
+            g = torch.Generator(device=t.device)
             g.manual_seed(1000 + idx)
-            view.normal_(0.0, 0.02, generator=g)
+            t.normal_(0.0, 0.02, generator=g)
+
+
+def fill_opt_buffer_device(buf, w):
+    """Fill a flat device tensor with the OPT-shaped synthetic weights, the tensors laid out back
+    to back in order (the same values as fill_opt_tensors_device on separate tensors)."""
+    views = [buf[o:o + sz] for _, o, sz in tensor_offsets(w)]
+    fill_opt_tensors_device(views, w)
 
 
 def stiff_paraboloid(d, kappa, seed):
