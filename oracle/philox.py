@@ -14,7 +14,7 @@ bumped by the Weyl constants (W0, W1) after every round (mod 2^W).
 
 The 1.5-SPSA paper does not state which generator produces its packed perturbations
 (section 4.3, "Bit-Packed perturbations"; Algorithm 1, PackedPerturbation). Philox4x32
-with 10 rounds is this build's reading; the round count is a parameter here.
+with 10 rounds is the reading taken here; the round count is a parameter.
 
 Pins: at W = 64, R = 10 this function must reproduce numpy.random.Philox bit for bit
 (numpy advances the counter by one before each block); at W = 32, R = 10 it must
