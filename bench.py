@@ -11,6 +11,8 @@ Prints one JSON line. `value` is the step's effective HBM bandwidth: algorithmic
 `fused_schedule` times the same step in 2K + 1 sweeps (zo_perturb2 merges the restore of
 probe k with the +eps of probe k + 1, zo_update_restore merges the last restore with the
 update) over the same number of steps.
+`graph_fused_schedule` replays the fused step captured once into a HIP graph (no host
+launches between kernels; each replay re-applies the captured step).
 Per-kernel durations come from HIP events recorded around every launch on the stream the
 kernels run on; `roofline` is the dominant kernel's (zo_perturb: 3K of the 3K + 1 sweeps)
 and `roofline_update` the fused update's.
@@ -154,6 +156,7 @@ def main():
 
     seed = 2024
     stream = torch.cuda.current_stream(dev)
+    cur = {"s": stream}  # the stream the sweeps are issued on (the capture stream while capturing)
     if args.layout == "flat":
         theta = torch.empty(n, dtype=dt, device=dev)
         if w.hidden:
@@ -161,23 +164,24 @@ def main():
         else:
             theta.copy_(torch.from_numpy(workloads.tiny_theta(n)))
         n_tensors = 1
-        perturb = lambda k, e, step: zo.zo_perturb(theta, k, e, seed, step, stream=stream)
-        perturb2 = lambda ka, ea, kb, eb, step: zo.zo_perturb2(theta, ka, ea, kb, eb, seed, step, stream=stream)
-        update = lambda c, step: zo.zo_update(theta, c, w.lr, seed, step, stream=stream)
+        perturb = lambda k, e, step: zo.zo_perturb(theta, k, e, seed, step, stream=cur["s"])
+        perturb2 = lambda ka, ea, kb, eb, step: zo.zo_perturb2(theta, ka, ea, kb, eb, seed, step, stream=cur["s"])
+        update = lambda c, step: zo.zo_update(theta, c, w.lr, seed, step, stream=cur["s"])
         update_restore = lambda c, step, kr, er: zo.zo_update_restore(theta, c, w.lr, seed, step, kr, er,
-                                                                      stream=stream)
+                                                                      stream=cur["s"])
     else:
         spans = workloads.tensor_offsets(w)
         tensors = [torch.empty(sz, dtype=dt, device=dev) for _, _, sz in spans]
         offs = [o for _, o, _ in spans]
         workloads.fill_opt_tensors_device(tensors, w)
         n_tensors = len(tensors)
-        perturb = lambda k, e, step: zo.zo_perturb_segments(tensors, offs, k, e, 0, 0.0, seed, step, stream=stream)
+        perturb = lambda k, e, step: zo.zo_perturb_segments(tensors, offs, k, e, 0, 0.0, seed, step,
+                                                            stream=cur["s"])
         perturb2 = lambda ka, ea, kb, eb, step: zo.zo_perturb_segments(tensors, offs, ka, ea, kb, eb, seed, step,
-                                                                       stream=stream)
-        update = lambda c, step: zo.zo_update_segments(tensors, offs, c, w.lr, seed, step, stream=stream)
+                                                                       stream=cur["s"])
+        update = lambda c, step: zo.zo_update_segments(tensors, offs, c, w.lr, seed, step, stream=cur["s"])
         update_restore = lambda c, step, kr, er: zo.zo_update_segments(tensors, offs, c, w.lr, seed, step, kr, er,
-                                                                       stream=stream)
+                                                                       stream=cur["s"])
         log(f"per-tensor layout: {n_tensors} separately allocated tensors")
     torch.cuda.synchronize()
     if args.calib_copy_gib > 0:
@@ -245,6 +249,25 @@ def main():
     torch.cuda.synchronize()
     fused_elapsed = time.perf_counter() - t0
     log(f"timed {args.steps} fused-schedule steps in {fused_elapsed:.3f} s")
+
+    # The fused step captured once into a HIP graph and replayed: every replay applies the
+    # captured step (its probes and coefficients) again, with no host launches in between.
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(stream)
+    torch.cuda.synchronize()
+    cur["s"] = side
+    with torch.cuda.graph(graph, stream=side):
+        fused_step(args.warmup + 2 * args.steps + 1)
+    cur["s"] = stream
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_elapsed = time.perf_counter() - t0
+    log(f"timed {args.steps} graph replays of the fused step in {graph_elapsed:.3f} s")
 
     # Plain in-place read-modify-write ceiling of the flat buffer (an even number of XOR passes
     # leaves the weights as they were). Not measured for the per-tensor layout, where a plain
@@ -358,6 +381,13 @@ def main():
             "effective_gbps": round((2 * K + 1) * sweep_bytes / (fused_elapsed / args.steps) / 1e9, 1),
             "speedup_vs_sequential": round(elapsed / fused_elapsed, 3),
             "step_params_probes_per_s": float(f"{n * 4 * K / (fused_elapsed / args.steps):.4e}"),
+        },
+        "graph_fused_schedule": {
+            "ms_per_step": round(graph_elapsed / args.steps * 1e3, 3),
+            "effective_gbps": round((2 * K + 1) * sweep_bytes / (graph_elapsed / args.steps) / 1e9, 1),
+            "speedup_vs_eager_fused": round(fused_elapsed / graph_elapsed, 3),
+            "how": "the fused step captured once into a HIP graph (torch.cuda.CUDAGraph) and replayed; "
+                   "each replay re-applies the captured step",
         },
     }
     out.update(baselines)
