@@ -186,8 +186,8 @@ int zo_update_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, 
  * tile_begin + n_tiles - 1 for probe group `group` (probes 8*group .. 8*group+7) to
  * out_dev (device memory, 16 * n_tiles bytes, caller-owned). Exposes the generator for
  * bit-exact checks; the sweeps never store probes.
- * Errors: ZO_ERR_NULL (out_dev NULL with n_tiles > 0), ZO_ERR_ARG (tile index overflow
- * past 2^60), ZO_ERR_HIP.
+ * Errors: ZO_ERR_NULL (out_dev NULL with n_tiles > 0), ZO_ERR_ARG (out_dev not 16-byte
+ * aligned, or tile indices reaching 2^60, the tile of element index 2^64), ZO_ERR_HIP.
  */
 int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_t seed,
                 uint32_t step, uint32_t group, void* stream);

@@ -8,6 +8,8 @@ to nearly zero the fp32 rounding of the operands can exceed a bf16 ulp of the re
 coefficients bit-exact (host tests).
 """
 
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -96,6 +98,20 @@ PERTURB_CASES = [
     (1, 0, 0, 1e-3), (15, 0, 1, 1e-3), (16, 0, 7, -2e-3), (17, 0, 8, 1e-3), (1000, 3, 63, 1e-4),
     (65_536 + 13, 0, 1000, 1e-3), (4099, 2 ** 35 + 7, 5, -2e-3), (300_000, 16, 17, 1e-3),
 ]
+
+
+def test_gen_bits_known_answer():
+    """Tile 0, seed 0, step 0, group 0 is Philox4x32-10 on the all-zero counter and key: the
+    block equals the published known-answer output (the other known-answer inputs lie outside
+    the library's index range)."""
+    golden = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "philox4x32_10_kat.txt")
+    rows = [[int(x, 16) for x in ln.split()] for ln in open(golden) if ln.strip() and not ln.startswith("#")]
+    want = np.array(rows[0][6:10], dtype=np.uint32)
+    assert rows[0][:6] == [0] * 6
+    out = torch.zeros(16, dtype=torch.uint8, device=DEV)
+    zo.zo_gen_bits(out, 0, 0, 0, 0)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint32), want)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
