@@ -39,6 +39,11 @@ LDS_PEAK_GLOOKUPS = 256 * 32 * 2.4  # 1e9 lookups/s
 LDS_RANDOM_GLOOKUPS = 256 * 64 / 6.31 * 2.4
 
 
+def workloads_names():
+    import workloads
+    return workloads.WORKLOADS.keys()
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -115,7 +120,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="opt13b", help="tiny, opt125m, opt1.3b, opt13b or opt30b")
+    ap.add_argument("--workload", default="opt13b", choices=sorted(workloads_names()),
+                    help="tiny, opt125m, opt1.3b, opt13b, opt30b, qwen3-1.7b or qwen3-8b")
     ap.add_argument("--K", type=int, default=0, help="probes per step (default: the workload's first)")
     ap.add_argument("--layout", default="flat", choices=["flat", "tensors"],
                     help="flat: one contiguous buffer (zo_perturb, zo_update); tensors: every OPT tensor "
@@ -134,7 +140,7 @@ def main():
     w = workloads.WORKLOADS[args.workload]
     K = args.K or w.K[0]
     if args.layout == "tensors" and not w.hidden:
-        print(f"--layout tensors needs an OPT-shaped workload ({w.name} is one flat vector)", file=sys.stderr)
+        print(f"--layout tensors needs a model-shaped workload ({w.name} is one flat vector)", file=sys.stderr)
         sys.exit(2)
     baselines = {}
     if not args.no_cpu_baseline:
@@ -160,7 +166,7 @@ def main():
     if args.layout == "flat":
         theta = torch.empty(n, dtype=dt, device=dev)
         if w.hidden:
-            workloads.fill_opt_buffer_device(theta, w)
+            workloads.fill_model_buffer_device(theta, w)
         else:
             theta.copy_(torch.from_numpy(workloads.tiny_theta(n)))
         n_tensors = 1
@@ -173,7 +179,7 @@ def main():
         spans = workloads.tensor_offsets(w)
         tensors = [torch.empty(sz, dtype=dt, device=dev) for _, _, sz in spans]
         offs = [o for _, o, _ in spans]
-        workloads.fill_opt_tensors_device(tensors, w)
+        workloads.fill_model_tensors_device(tensors, w)
         n_tensors = len(tensors)
         perturb = lambda k, e, step: zo.zo_perturb_segments(tensors, offs, k, e, 0, 0.0, seed, step,
                                                             stream=cur["s"])

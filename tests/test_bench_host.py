@@ -29,7 +29,7 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 def test_per_tensor_layout_needs_an_opt_workload():
     r = _run("--workload", "tiny", "--layout", "tensors", "--no-cpu-baseline")
     assert r.returncode == 2
-    assert "OPT-shaped" in r.stderr
+    assert "model-shaped" in r.stderr
 
 
 def test_committed_counters_match_the_sweep_source():

@@ -575,7 +575,8 @@ def _windows(n, rng, count, size, boundaries=()):
     return sorted({min(max(s, 0), n - 1) for s in starts})
 
 
-@pytest.mark.parametrize("name,K", [("opt125m", 16), ("opt13b", 16), ("opt1.3b", 64), ("opt30b", 32)])
+@pytest.mark.parametrize("name,K", [("opt125m", 16), ("opt13b", 16), ("opt1.3b", 64), ("opt30b", 32),
+                                    ("qwen3-1.7b", 60), ("qwen3-8b", 60)])
 def test_full_size_sampled_windows(name, K):
     """At the full OPT-shaped size, in the benchmark's launch configuration, on 32 random
     windows of 2^20 weights plus the first window, the last (with the ragged tail) and windows
@@ -586,7 +587,7 @@ def test_full_size_sampled_windows(name, K):
     n = w.n
     note(f"full-size {name}: n {n} K {K}")
     buf = torch.empty(n, dtype=torch.bfloat16, device=DEV)
-    workloads.fill_opt_buffer_device(buf, w)
+    workloads.fill_model_buffer_device(buf, w)
     rng = np.random.default_rng(7)
     offs = [o for _, o, _ in workloads.tensor_offsets(w)]
     bounds = [offs[1], offs[2], offs[len(offs) // 2], offs[-2]]
@@ -633,7 +634,7 @@ def test_full_size_separate_tensors():
     note(f"full-size opt13b as {len(spans)} tensors")
     tensors = [torch.empty(sz, dtype=torch.bfloat16, device=DEV) for _, _, sz in spans]
     offs = [o for _, o, _ in spans]
-    workloads.fill_opt_tensors_device(tensors, w)
+    workloads.fill_model_tensors_device(tensors, w)
     rng = np.random.default_rng(11)
     pick = {0, len(spans) - 1, int(np.argmax([sz for _, _, sz in spans]))}
     pick |= {int(i) for i in rng.integers(0, len(spans), 24)}
