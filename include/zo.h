@@ -25,9 +25,11 @@
  *   - stream: a hipStream_t (NULL = the default stream). Device work is enqueued on it
  *     and the call returns without waiting; faults surface at the caller's next
  *     synchronisation. Host arguments (coefficient arrays) are copied before return.
- *   - Errors: every argument is validated before anything is launched; on a negative
- *     status nothing was enqueued and no output was written. n = 0 (or K = 0) is a
- *     successful no-op.
+ *   - Errors: every argument is validated before anything is launched; on ZO_ERR_NULL,
+ *     ZO_ERR_ARG or ZO_ERR_NONFINITE nothing was enqueued and no output was written.
+ *     ZO_ERR_HIP reports a launch the runtime refused (for the segment calls, earlier
+ *     batches of the same call may already be enqueued). n = 0 (or K = 0) is a successful
+ *     no-op.
  *   - No global state is kept between calls except an optional launch-width override
  *     (zo_set_max_blocks); calls on different streams may run concurrently on disjoint
  *     parameter memory. The library allocates no device memory.

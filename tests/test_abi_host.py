@@ -7,6 +7,7 @@ zo_probe_coeffs is host code.
 import ctypes
 import os
 import re
+import subprocess
 
 import numpy as np
 import pytest
@@ -186,3 +187,22 @@ def test_binding_refuses_cpu_tensors(lib):
     import torch
     with pytest.raises(TypeError):
         zo.zo_perturb(torch.zeros(4), 0, 1e-3, 0, 0)
+
+
+def test_plain_c_consumer(tmp_path):
+    """The header compiles as C99 with warnings as errors, and a C program linked against
+    libzo.so gets the documented host results and validation codes (no GPU needed)."""
+    import shutil
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    exe = tmp_path / "abi_c_check"
+    src = os.path.join(ROOT, "tests", "helpers", "abi_c_check.c")
+    libdir = os.path.dirname(zo.LIB_PATH)
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-I", os.path.join(ROOT, "include"), src,
+                        "-o", str(exe), "-L", libdir, "-lzo", "-Wl,-rpath," + libdir, "-lm"],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.count("ok ") == 15 and "FAIL" not in r.stdout, r.stdout
