@@ -97,6 +97,9 @@ PERTURB_CASES = [
     # n, offset, k, eps
     (1, 0, 0, 1e-3), (15, 0, 1, 1e-3), (16, 0, 7, -2e-3), (17, 0, 8, 1e-3), (1000, 3, 63, 1e-4),
     (65_536 + 13, 0, 1000, 1e-3), (4099, 2 ** 35 + 7, 5, -2e-3), (300_000, 16, 17, 1e-3),
+    # the top of both index ranges: last global elements below 2^64, the last probe 2^32 - 1
+    # (odd offsets take the element path, 2^64 - 2^17 the vector path)
+    (5_000, 2 ** 64 - 5_001, 2 ** 32 - 1, 1e-3), (2 ** 17 - 1, 2 ** 64 - 2 ** 17, 2 ** 32 - 9, -2e-3),
 ]
 
 
@@ -220,6 +223,8 @@ UPDATE_CASES = [
     (20_000, 2 ** 33 + 1, 0, 24), (20_000, 0, 0, 32), (50_000, 0, 0, 64), (9_000, 0, 0, 65),
     (5_000, 0, 0, 200), (3_000, 0, 0, 256), (10_000, 48, 3, 16), (10_000, 0, 8, 16), (7_000, 0, 100, 57),
     (4_100, 0, 0, 512), (3_000, 17, 0, 1024), (2_500, 0, 5, 1024),
+    (6_000, 2 ** 64 - 6_001, 2 ** 32 - 40, 40), (5_000, 2 ** 60, 2 ** 32 - 64, 64),
+    (2 ** 17 - 1, 2 ** 64 - 2 ** 17, 2 ** 32 - 24, 24),
 ]
 
 
