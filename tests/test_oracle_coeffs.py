@@ -1,5 +1,6 @@
 """Pins of the coefficient function: exact quadratic curvature, the paper's special cases."""
 
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -67,11 +68,16 @@ def test_alpha_zero_is_1spsa():
 
 
 def test_worked_value_curvature_1e8():
-    """Section 6: a curvature of 1e8 with alpha = 0.1 is down-weighted by about 6.3."""
+    """Section 6's worked value (tests/golden/curvature_weight_worked_value.txt): a
+    three-point curvature of 1e8 with alpha = 0.1 is down-weighted by the printed factor."""
+    golden = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "curvature_weight_worked_value.txt")
+    row = [ln.split() for ln in open(golden) if ln.strip() and not ln.startswith("#")][0]
+    curv, alpha, factor, tol = (float(x) for x in row)
     eps = 1e-3
-    co = oracle.probe_coeffs([52.0], [50.0], 1.0, eps)
-    assert abs(co["curv"][0] - 1e8) < 1e-3
-    assert abs(1.0 / co["w"][0] - 6.3) < 0.05
+    # L+ - 2 L0 + L- = curv * eps^2 = 100 with L0 = 1
+    co = oracle.probe_coeffs([52.0], [50.0], 1.0, eps, alpha=alpha)
+    assert abs(co["curv"][0] - curv) < 1e-3
+    assert abs(1.0 / co["w"][0] - factor) < tol
 
 
 def test_saturation_below_lambda():
