@@ -100,11 +100,18 @@ def _check(status, what):
 
 
 def _stream(theta_or_device, stream):
+    """The hipStream_t to launch on: torch's current stream of the tensor's device, or the
+    given stream (a torch stream, which must belong to that device, or a raw handle)."""
     import torch
+    dev = theta_or_device.device if hasattr(theta_or_device, "device") else theta_or_device  # None: no tensors
     if stream is None:
-        dev = theta_or_device.device if hasattr(theta_or_device, "device") else theta_or_device
         return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
-    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    if hasattr(stream, "cuda_stream"):
+        sdev = getattr(stream, "device", None)
+        if dev is not None and sdev is not None and torch.device(sdev) != torch.device(dev):
+            raise ValueError(f"the stream belongs to {sdev}, the tensors to {dev}")
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
 
 
 def _theta_args(theta):
@@ -145,7 +152,6 @@ def zo_update_restore(theta, c, lr, seed, step, k_restore, eps_restore, offset=0
 
 
 def _segments(tensors, offsets):
-    import torch
     tensors = list(tensors)
     if len(tensors) != len(offsets):
         raise ValueError("one global offset per tensor")
@@ -160,7 +166,7 @@ def _segments(tensors, offsets):
     for i, (t, o) in enumerate(zip(tensors, offsets)):
         p, dt, n = _theta_args(t)
         arr[i] = ZoSegment(p, int(o), n)
-    return arr, len(tensors), dt, (tensors[0] if tensors else torch.device("cuda"))
+    return arr, len(tensors), dt, (tensors[0] if tensors else None)
 
 
 def zo_perturb_segments(tensors, offsets, k_a, eps_a, k_b, eps_b, seed, step, stream=None):

@@ -304,6 +304,10 @@ def test_empty_and_noop_calls():
     assert torch.equal(u, before)
     with pytest.raises(zo.ZoError):
         zo.zo_update(u, np.zeros(zo.ZO_K_MAX + 1, np.float32), 1e-3, 0, 0)
+    side = torch.cuda.Stream()
+    zo.zo_perturb_segments([], [], 0, 1e-3, 0, 0.0, 0, 0, stream=side)  # an empty list on a given stream
+    zo.zo_update_segments([], [], [1.0], 1e-3, 0, 0, stream=side)
+    zo.zo_perturb_segments([u[:0]], [0], 0, 1e-3, 0, 0.0, 0, 0)  # an empty tensor
     torch.cuda.synchronize()
     assert torch.equal(u, before)
 
