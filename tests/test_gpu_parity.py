@@ -559,6 +559,32 @@ def test_graph_capture_replays_match_eager(dtype):
         np.testing.assert_array_equal(bits(g), bits(a), err_msg=f"replay {replay}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sharded_calls_equal_the_full_buffer(dtype):
+    """The element-range sharding of a model too large for one device: each shard is stepped
+    by its own calls with its global offset (uneven cuts, some mid-tile and mid-chunk), and the
+    concatenation equals the full-buffer calls bit for bit (perturb, two-probe transition,
+    update with restore)."""
+    n = 1_000_003
+    cuts = [0, 123_457, 123_460, 600_001, n]
+    h = workloads.normal_f32(n, 40) if dtype == "f32" else workloads.normal_bf16_bits(n, 40)
+    dev = (lambda x: torch.from_numpy(x).to(DEV)) if dtype == "f32" else to_dev_bf16
+    full, sharded = dev(h), dev(h)
+    c = np.random.default_rng(9).standard_normal(24).astype(np.float32)
+    seed, step, eps, lr = 5, 2, 1e-3, 1e-3
+    zo.zo_perturb(full, 3, eps, seed, step)
+    zo.zo_perturb2(full, 3, -2 * eps, 4, eps, seed, step)
+    zo.zo_update_restore(full, c, lr, seed, step, 4, -eps)
+    for a, b in zip(cuts, cuts[1:]):
+        shard = sharded[a:b]
+        zo.zo_perturb(shard, 3, eps, seed, step, offset=a)
+        zo.zo_perturb2(shard, 3, -2 * eps, 4, eps, seed, step, offset=a)
+        zo.zo_update_restore(shard, c, lr, seed, step, 4, -eps, offset=a)
+    torch.cuda.synchronize()
+    bits = (lambda t: t.cpu().numpy().view(np.uint32)) if dtype == "f32" else host_bits
+    np.testing.assert_array_equal(bits(sharded), bits(full))
+
+
 # ----------------------------------------------------------------------------- full step
 def test_full_tiny_step():
     """The tiny fp32 workload: 2^20 weights, K = 4, eps 1e-3, lr 1e-4 (schedule + coeffs + update)."""
