@@ -1,8 +1,8 @@
 /* zo_calib.h - measurement aid shipped beside libzo (libzo_calib.so); not part of the method.
  *
- * The probe sweeps are bound by HBM read-modify-write bandwidth, and on MI355X that ceiling
- * depends on where a buffer sits physically (the same kernel reaches different rates on
- * different allocations). zo_calib_rmw gives the plain ceiling of a given buffer, so a sweep's
+ * The probe sweeps are bound by HBM read-modify-write bandwidth, which on MI355X depends on
+ * the access pattern and, for some patterns, on where a buffer sits physically. zo_calib_rmw
+ * gives the plain ceiling of a given buffer in the sweeps' own access pattern, so a sweep's
  * rate can be reported as a fraction of it as well as of the nominal 8 TB/s.
  */
 #ifndef ZO_CALIB_H
@@ -15,9 +15,11 @@ extern "C" {
 #endif
 
 /* XOR every 16-byte vector of p[0 .. bytes) in place with `key` replicated four times:
- * one read and one write of every byte, in the memory shape of the sweep kernels (1 KiB per
- * wave instruction, non-temporal loads and stores, grid-stride, 65,536 x 256 threads) and no
- * other work. Two calls with the same key restore the buffer bit for bit.
+ * one read and one write of every byte, in the streaming shape of the perturb sweep (each
+ * wave walks up to 32 KiB in 2 KiB steps with the next two steps' loads in flight,
+ * non-temporal loads and stores, one workgroup of 256 threads per CU at a time, grid-stride
+ * over up to 65,536 workgroups) and no other work. Two calls with the same key restore the
+ * buffer bit for bit.
  *   p      caller-owned device memory, 16-byte aligned; bytes a multiple of 16.
  *   stream hipStream_t (NULL = default stream); the call is asynchronous on it.
  * Returns 0; -1 for p == NULL with bytes > 0; -2 for misalignment or a size that is not a

@@ -7,16 +7,19 @@
 // block per 16-element tile and probe group of 8, 8 probe signs per byte (section 4.3).
 // Nothing but theta touches HBM.
 //
-// Memory layout of a sweep. theta is streamed in chunks of 64 x kU contiguous 16-byte
-// vectors per wave: each load and store instruction of a wave covers 1 KiB of contiguous
-// memory (non-temporal: nothing is reused). A tile spans 2 vectors (bf16) or 4 (fp32); the
-// lanes holding one tile are m and m + 32 (bf16) or m, m + 16, m + 32, m + 48 (fp32), so
-// that the gfx950 half-wave swaps v_permlane32_swap / v_permlane16_swap exchange the
-// generator words: each lane runs Philox for kU / kLanesPerTile of the chunk's tiles, then
-// bf16 lane pairs swap two words per pair of blocks (two instructions) and fp32 lane groups
-// transpose a 4x4 word matrix (four instructions). Head and tail elements that do not fill a
-// chunk (and everything, when the storage is not 16-byte aligned relative to the global
-// index) take an element-wise path, one tile per lane.
+// Memory layout of a sweep. theta is walked in row groups of 1024 elements: 2 (bf16) or 4
+// (fp32) rows of 64 contiguous 16-byte vectors, one vector per lane and row, so each load and
+// store instruction of a wave covers 1 KiB of contiguous memory (non-temporal: nothing is
+// reused). A tile spans 2 vectors (bf16) or 4 (fp32); the lanes holding one tile are m and
+// m + 32 (bf16) or m, m + 16, m + 32, m + 48 (fp32), so that the gfx950 half-wave swaps
+// v_permlane32_swap / v_permlane16_swap exchange the generator words: each lane runs one
+// Philox block per row group and probe group, then bf16 lane pairs swap two words (two
+// instructions) and fp32 lane groups transpose a 4x4 word matrix (four instructions). A wave
+// streams a chunk of consecutive row groups (up to 32 KiB) with the loads of the next one or
+// two groups in flight while it works on the current one, and large sweeps cap the
+// workgroups per CU (few long read-write streams keep HBM busiest). Head and tail elements
+// that do not fill a row group (and everything, when the storage is not 16-byte aligned
+// relative to the global index) take an element-wise path, one tile per lane.
 //
 // zo_perturb_segments / zo_update_segments sweep a list of separate tensors: the host validates
 // the list, builds one plan per tensor and launches batches of up to 64 plans (kernel
@@ -45,7 +48,8 @@ namespace {
 constexpr uint32_t kTile = 16;    // elements per generator block
 constexpr uint32_t kBlock = 256;  // threads per workgroup (4 waves)
 constexpr uint32_t kWavesPerBlock = kBlock / 64;
-constexpr int kU = 4;             // 16-byte vectors per lane per chunk
+constexpr uint64_t kGroupElems = 1024;      // elements per row group (one Philox block per lane)
+constexpr uint64_t kMaxChunkBytes = 32768;  // bytes a wave streams per chunk, at most
 constexpr uint32_t kDefaultMaxBlocks = 65536;
 constexpr int kRounds = 10;
 
@@ -162,46 +166,47 @@ struct BF16 {
   }
 };
 
+// A row group: kRows rows of 64 contiguous 16-byte vectors (one vector per lane and row),
+// 1024 elements, i.e. one Philox block per lane and probe group.
 template <class S>
-struct ChunkShape {
-  static constexpr uint64_t kVecs = 64ull * kU;                      // vectors per chunk
-  static constexpr uint64_t kElems = kVecs * S::kVecElems;           // bf16 2048, fp32 1024
+struct GroupShape {
+  static constexpr int kRows = S::kLanesPerTile;                // bf16 2, fp32 4
+  static constexpr uint64_t kVecs = 64ull * kRows;
+  static constexpr uint64_t kElems = kVecs * S::kVecElems;
+  static constexpr uint64_t kBytes = kVecs * 16;                // bf16 2 KiB, fp32 4 KiB
+  static_assert(kElems == kGroupElems, "a row group holds 1024 elements");
 };
 
-// Chunk vector held by a lane (for every u, lane l holds chunk vector 64u + vec_of_lane(l)):
+// Group vector held by a lane (for every row u, lane l holds group vector 64u + vec_of_lane(l)):
 // the lanes of one tile sit 32 (bf16) or 16 (fp32) lanes apart.
 template <class S>
 __device__ __forceinline__ uint32_t vec_of_lane(uint32_t lane) {
   return S::kLanesPerTile == 2 ? 2 * (lane & 31u) + (lane >> 5) : 4 * (lane & 15u) + (lane >> 4);
 }
 
-// For chunk vector base vbase (a global vector index, multiple of 64 kU) and probe group g:
-// W[u][w] = the generator words this lane's vector u needs.
+// For a row group starting at global vector vbase (a multiple of GroupShape::kVecs) and probe
+// group g: W[u][w] = the generator words this lane's vector in row u needs.
 // bf16: lanes m and m + 32 hold the two halves of tile T(u) = vbase/2 + 32u + m; lane m + 32q
-// generates tiles 2j + q, and one permlane32 swap per word pair hands each lane the half it
+// generates tile T(q), and one permlane32 swap per word pair hands each lane the half it
 // needs (x,y for the first half, z,w for the second).
-__device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
-                                            uint32_t (&W)[kU][BF16::kWords], BF16) {
+__device__ __forceinline__ void group_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
+                                            uint32_t (&W)[2][BF16::kWords], BF16) {
   const uint32_t q = lane >> 5, m = lane & 31u;
-  const uint64_t t0 = vbase / 2 + m;
-#pragma unroll
-  for (int j = 0; j < kU / 2; ++j) {
-    const uint4 r = gen.block(t0 + 32ull * (2 * j + q), group);
-    const auto sx = __builtin_amdgcn_permlane32_swap(r.x, r.z, false, false);
-    const auto sy = __builtin_amdgcn_permlane32_swap(r.y, r.w, false, false);
-    W[2 * j][0] = sx[0];
-    W[2 * j][1] = sy[0];
-    W[2 * j + 1][0] = sx[1];
-    W[2 * j + 1][1] = sy[1];
-  }
+  const uint4 r = gen.block(vbase / 2 + 32ull * q + m, group);
+  const auto sx = __builtin_amdgcn_permlane32_swap(r.x, r.z, false, false);
+  const auto sy = __builtin_amdgcn_permlane32_swap(r.y, r.w, false, false);
+  W[0][0] = sx[0];
+  W[0][1] = sy[0];
+  W[1][0] = sx[1];
+  W[1][1] = sy[1];
 }
 
 // fp32: lanes m + 16q (q = 0..3) hold the four quarters of tile T(u) = vbase/4 + 16u + m;
 // lane m + 16q generates tile T(q), and a 4x4 transpose across the four lanes (permlane32
 // swaps exchange the off-diagonal 2x2 blocks, permlane16 swaps the elements inside them)
 // leaves word q of tile T(u) in register u.
-__device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
-                                            uint32_t (&W)[kU][F32::kWords], F32) {
+__device__ __forceinline__ void group_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
+                                            uint32_t (&W)[4][F32::kWords], F32) {
   const uint32_t q = lane >> 4, m = lane & 15u;
   const uint4 r = gen.block(vbase / 4 + 16ull * q + m, group);
   uint32_t a[4] = {r.x, r.y, r.z, r.w};
@@ -220,7 +225,7 @@ __device__ __forceinline__ void chunk_words(const Gen& gen, uint64_t vbase, uint
   sw16(0, 1);
   sw16(2, 3);
 #pragma unroll
-  for (int u = 0; u < kU; ++u) W[u][0] = a[u];
+  for (int u = 0; u < 4; ++u) W[u][0] = a[u];
 }
 
 // Probe byte of element e (0 .. kVecElems-1) of a vector, from its words.
@@ -246,11 +251,14 @@ __device__ __forceinline__ void tile_elementwise(typename S::storage* params, ui
 }
 
 // One segment: global elements [lo, hi) stored from `base` (the address of global element lo).
-// Full chunks [c_first, c_first + n_chunks) take the vector path; the edge tiles
-// [head_t0, +head_nt) and [tail_t0, +tail_nt) take the element-wise path.
+// The full row groups [g_lo, g_hi) (global group indices) take the vector path, in chunks of
+// up to `chunk_groups` groups aligned to multiples of chunk_groups: chunks
+// [c_first, c_first + n_chunks) meet the range. The edge tiles [head_t0, +head_nt) and
+// [tail_t0, +tail_nt) (fewer than 1024 elements at each end) take the element-wise path.
 struct Plan {
   char* base;
   uint64_t lo, hi;
+  uint64_t g_lo, g_hi;
   uint64_t c_first, n_chunks;
   uint64_t head_t0, head_nt, tail_t0, tail_nt;
 };
@@ -260,40 +268,107 @@ struct Plan {
 template <int N>
 struct Plans {
   uint32_t count;
+  uint32_t chunk_groups;
   uint64_t chunk_end[N];
   uint64_t edge_end[N];
   Plan p[N];
 };
 
 template <class S>
-__device__ __forceinline__ void load_chunk(u32x4 (&d)[kU], const char* base, uint32_t lane) {
+__device__ __forceinline__ void load_group(u32x4 (&d)[GroupShape<S>::kRows], const char* base, uint32_t lane) {
   const uint32_t v = vec_of_lane<S>(lane);
 #pragma unroll
-  for (int u = 0; u < kU; ++u) d[u] = ld_stream(base + 16 * (64 * u + v));
+  for (int u = 0; u < GroupShape<S>::kRows; ++u) d[u] = ld_stream(base + 16 * (64 * u + v));
 }
 
 template <class S>
-__device__ __forceinline__ void store_chunk(char* base, const u32x4 (&d)[kU], uint32_t lane) {
+__device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupShape<S>::kRows], uint32_t lane) {
   const uint32_t v = vec_of_lane<S>(lane);
 #pragma unroll
-  for (int u = 0; u < kU; ++u) st_stream(base + 16 * (64 * u + v), d[u]);
+  for (int u = 0; u < GroupShape<S>::kRows; ++u) st_stream(base + 16 * (64 * u + v), d[u]);
 }
 
-// Calls body(vbase, base) for every full chunk of the launch, one wave per chunk, where
-// vbase is the chunk's global vector index and base its byte address. A wave's chunk
-// indices increase, so its segment cursor only moves forward.
-template <class S, int N, class Body>
-__device__ __forceinline__ void for_each_chunk(const Plans<N>& ps, Body body) {
+// Calls body(vbase, d, lane) for every full row group of the launch, where vbase is the
+// group's global vector index and d its data, and stores what the body leaves in d. One
+// wave per chunk walks the chunk's groups in address order with the loads of the next AHEAD
+// groups in flight while the body works on the current one (each wave streams up to 32 KiB,
+// reads and writes interleaved; two ahead pays for the light perturb, one for the update). A
+// wave's chunk indices increase, so its segment cursor only moves forward.
+template <class S, int AHEAD, int N, class Body>
+__device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
+  static_assert(AHEAD == 1 || AHEAD == 2, "one or two groups in flight");
+  using G = GroupShape<S>;
   const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
   const uint64_t total = ps.chunk_end[ps.count - 1];
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint64_t cg = ps.chunk_groups;
   uint32_t s = 0;
   for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + wave; c < total; c += n_waves) {
     while (c >= ps.chunk_end[s]) ++s;
     const Plan& pl = ps.p[s];
     const uint64_t chunk = pl.c_first + (c - (s ? ps.chunk_end[s - 1] : 0));
-    char* base = pl.base + (chunk * ChunkShape<S>::kElems - pl.lo) * sizeof(typename S::storage);
-    body(chunk * ChunkShape<S>::kVecs, base);
+    const uint64_t g0 = chunk * cg > pl.g_lo ? chunk * cg : pl.g_lo;
+    const uint64_t g1 = chunk * cg + cg < pl.g_hi ? chunk * cg + cg : pl.g_hi;
+    char* base = pl.base + (g0 * kGroupElems - pl.lo) * sizeof(typename S::storage);
+    // Rotating register sets: while the body works on one group, the loads of the next AHEAD
+    // groups are in flight. No register of an outstanding load is ever copied, and inside the
+    // loops the prefetches do not depend on a branch (either would make the compiler wait
+    // for every outstanding load before the work).
+    u32x4 x[G::kRows], y[G::kRows], z[G::kRows];
+    auto work = [&](u32x4 (&cur)[G::kRows], uint64_t g) {
+      body(g * G::kVecs, cur, lane);
+      store_group<S>(base, cur, lane);
+      base += G::kBytes;
+    };
+    auto prefetch = [&](u32x4 (&nxt)[G::kRows], uint64_t ahead) {
+      load_group<S>(nxt, base + ahead * G::kBytes, lane);
+      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the work (the scheduler sinks it)
+    };
+    load_group<S>(x, base, lane);
+    uint64_t g = g0;
+    if constexpr (AHEAD == 1) {
+      for (; g + 2 < g1; g += 2) {  // at least three groups left: two steps that both prefetch
+        prefetch(y, 1);
+        work(x, g);
+        prefetch(x, 1);
+        work(y, g + 1);
+      }
+      if (g + 1 < g1) {  // two groups left
+        prefetch(y, 1);
+        work(x, g);
+        work(y, g + 1);
+      } else {
+        work(x, g);
+      }
+    } else {
+      if (g + 1 < g1) load_group<S>(y, base + G::kBytes, lane);
+      for (; g + 4 < g1; g += 3) {  // at least five groups left: three steps that prefetch two ahead
+        prefetch(z, 2);
+        work(x, g);
+        prefetch(x, 2);
+        work(y, g + 1);
+        prefetch(y, 2);
+        work(z, g + 2);
+      }
+      const uint64_t left = g1 - g;  // 1 to 4; x (and y when left > 1) requested
+      if (left >= 3) {
+        prefetch(z, 2);
+        work(x, g);
+        if (left == 4) {
+          prefetch(x, 2);
+          work(y, g + 1);
+          work(z, g + 2);
+          work(x, g + 3);
+        } else {
+          work(y, g + 1);
+          work(z, g + 2);
+        }
+      } else {
+        work(x, g);
+        if (left == 2) work(y, g + 1);
+      }
+    }
   }
 }
 
@@ -322,25 +397,25 @@ struct Probe {
 
 template <class S, bool TWO, int N>
 __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, Probe a, Probe b) {
-  const uint32_t lane = threadIdx.x & 63u;
+  extern __shared__ uint32_t occupancy_pad[];  // dynamic LDS only limits workgroups per CU
+  if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count <= 64)
+  constexpr int R = GroupShape<S>::kRows;
   const bool shared_group = a.group == b.group;
-  for_each_chunk<S>(ps, [&](uint64_t vbase, char* base) {
-    u32x4 d[kU];
-    load_chunk<S>(d, base, lane);
-    uint32_t Wa[kU][S::kWords], Wb[kU][S::kWords];
-    chunk_words(gen, vbase, lane, a.group, Wa, S());
+  for_each_group<S, 2>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+    uint32_t Wa[R][S::kWords], Wb[R][S::kWords];
+    group_words(gen, vbase, lane, a.group, Wa, S());
     if (TWO) {
       if (shared_group) {
 #pragma unroll
-        for (int u = 0; u < kU; ++u)
+        for (int u = 0; u < R; ++u)
 #pragma unroll
           for (int q = 0; q < S::kWords; ++q) Wb[u][q] = Wa[u][q];
       } else {
-        chunk_words(gen, vbase, lane, b.group, Wb, S());
+        group_words(gen, vbase, lane, b.group, Wb, S());
       }
     }
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
+    for (int u = 0; u < R; ++u) {
       float v[S::kVecElems];
       S::unpack(d[u], v);
 #pragma unroll
@@ -351,7 +426,6 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
       }
       d[u] = S::pack(v);
     }
-    store_chunk<S>(base, d, lane);
   });
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     const uint4 ra = gen.block(t, a.group);
@@ -396,15 +470,17 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
   __syncthreads();
 }
 
-// acc[u][e] (+)= table value of group g for each element of the chunk.
+// acc[u][e] (+)= table value of probe group g for each element of the row group.
 template <class S, bool FIRST>
-__device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
-                                          uint64_t vbase, uint32_t lane, uint32_t g, uint32_t g_first) {
-  uint32_t W[kU][S::kWords];
-  chunk_words(gen, vbase, lane, g_first + g, W, S());
+__device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
+                                          const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t g,
+                                          uint32_t g_first) {
+  constexpr int R = GroupShape<S>::kRows;
+  uint32_t W[R][S::kWords];
+  group_words(gen, vbase, lane, g_first + g, W, S());
   const float* tg = tab + 256u * g;
 #pragma unroll
-  for (int u = 0; u < kU; ++u)
+  for (int u = 0; u < R; ++u)
 #pragma unroll
     for (int e = 0; e < S::kVecElems; ++e) {
       const float x = table_at(tg, W[u][e >> 2], e & 3);
@@ -412,24 +488,26 @@ __device__ __forceinline__ void add_group(float (&acc)[kU][S::kVecElems], const 
     }
 }
 
-// Sum of the tables of groups 0 .. n_groups-1 for the chunk: NG > 0 fixes the count at
-// compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
+// Sum of the tables of probe groups 0 .. n_groups-1 for the row group: NG > 0 fixes the count
+// at compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
 template <class S, int NG>
-__device__ __forceinline__ void chunk_sums(float (&acc)[kU][S::kVecElems], const float* tab, const Gen& gen,
-                                           uint64_t vbase, uint32_t lane, uint32_t n_groups, uint32_t g_first) {
+__device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
+                                           const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t n_groups,
+                                           uint32_t g_first) {
+  constexpr int R = GroupShape<S>::kRows;
   if constexpr (NG > 0) {
     add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first);
 #pragma unroll
     for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first);
   } else {
-    float comp[kU][S::kVecElems];
+    float comp[R][S::kVecElems];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
-      float part[kU][S::kVecElems];
+      float part[R][S::kVecElems];
       add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first);
       const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
       for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first);
 #pragma unroll
-      for (int u = 0; u < kU; ++u)
+      for (int u = 0; u < R; ++u)
 #pragma unroll
         for (int e = 0; e < S::kVecElems; ++e) {
           if (g0 == 0) {
@@ -443,7 +521,7 @@ __device__ __forceinline__ void chunk_sums(float (&acc)[kU][S::kVecElems], const
         }
     }
 #pragma unroll
-    for (int u = 0; u < kU; ++u)
+    for (int u = 0; u < R; ++u)
 #pragma unroll
       for (int e = 0; e < S::kVecElems; ++e) acc[u][e] = acc[u][e] + comp[u][e];
   }
@@ -495,16 +573,14 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   build_tables(tab, cf, k_base, K, n_groups);
   const uint32_t g_first = k_base / 8;
-  const uint32_t lane = threadIdx.x & 63u;
-  for_each_chunk<S>(ps, [&](uint64_t vbase, char* base) {
-    u32x4 d[kU];
-    load_chunk<S>(d, base, lane);
-    float acc[kU][S::kVecElems];
-    chunk_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
-    uint32_t Wr[kU][S::kWords];  // the restore probe's generator words
-    if (RESTORE) chunk_words(gen, vbase, lane, r.group, Wr, S());
+  constexpr int R = GroupShape<S>::kRows;
+  for_each_group<S, 1>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+    float acc[R][S::kVecElems];
+    group_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
+    uint32_t Wr[R][S::kWords];  // the restore probe's generator words
+    if (RESTORE) group_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
+    for (int u = 0; u < R; ++u) {
       float v[S::kVecElems];
       S::unpack(d[u], v);
 #pragma unroll
@@ -514,7 +590,6 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
       }
       d[u] = S::pack(v);
     }
-    store_chunk<S>(base, d, lane);
   });
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
@@ -562,9 +637,9 @@ int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n) {
 
 uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
 
-// Full chunks need the address of global element 0 (params shifted back by offset
-// elements) to be 16-byte aligned, so that every chunk vector is an aligned 16 bytes.
-Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t chunk_elems) {
+// Full row groups need the address of global element 0 (params shifted back by offset
+// elements) to be 16-byte aligned, so that every group vector is an aligned 16 bytes.
+Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t chunk_groups) {
   Plan pl{};
   pl.base = static_cast<char*>(params);
   pl.lo = offset;
@@ -573,12 +648,14 @@ Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t 
   const uintptr_t base = reinterpret_cast<uintptr_t>(params) - static_cast<uintptr_t>(offset * elem);
   uint64_t head_end = pl.hi, tail_begin = pl.hi;
   if ((base & 15u) == 0) {
-    const uint64_t c0 = ceil_div(pl.lo, chunk_elems), c1 = pl.hi / chunk_elems;
-    if (c0 < c1) {
-      pl.c_first = c0;
-      pl.n_chunks = c1 - c0;
-      head_end = c0 * chunk_elems;
-      tail_begin = c1 * chunk_elems;
+    const uint64_t g_lo = ceil_div(pl.lo, kGroupElems), g_hi = pl.hi / kGroupElems;
+    if (g_lo < g_hi) {
+      pl.g_lo = g_lo;
+      pl.g_hi = g_hi;
+      pl.c_first = g_lo / chunk_groups;
+      pl.n_chunks = ceil_div(g_hi, chunk_groups) - pl.c_first;
+      head_end = g_lo * kGroupElems;
+      tail_begin = g_hi * kGroupElems;
     }
   }
   if (head_end > pl.lo) {
@@ -628,22 +705,73 @@ struct Sweep {
   bool restore;
 };
 
+// Streaming shape of a launch over `elements` weights of `elem` bytes. HBM sustains these
+// in-place sweeps best as few long sequential read-write streams: each wave walks up to
+// kMaxChunkBytes of consecutive row groups with the next group in flight, and occupancy is
+// capped so that few waves stream at once (measured on one buffer: 6.2 TB/s for the bf16
+// perturb at one workgroup per CU against 5.4 at full occupancy). The cap rises with the
+// generator work per byte, which a wave must hide behind its own loads: work = generator
+// blocks per row group, an update's probe group counting twice (block and table lookups),
+// doubled for bf16 (twice the elements per byte). Sweeps smaller than the 256 MiB Infinity
+// Cache keep 4 KiB chunks at full occupancy. Thresholds from measured sweeps of every kernel
+// over occupancy on OPT-1.3B and OPT-13B shaped bf16 and 3 G-element fp32 buffers; kernels
+// with more work (K >= 32 updates in bf16, K >= 48 in fp32) are bound by the generator or the
+// LDS and keep 4 KiB chunks at full occupancy.
+struct Shape {
+  uint32_t chunk_groups;
+  uint32_t blocks_per_cu;  // 0: no cap
+};
+
+constexpr uint64_t kStreamBytes = 256ull << 20;
+
+Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
+  const uint64_t group_bytes = kGroupElems * elem;
+  const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0};
+  if (elements * elem < kStreamBytes) return short_chunks;
+  const uint32_t units = w.update ? 2 * w.n_groups + (w.restore ? 1u : 0u) : (w.two && w.a.group != w.b.group ? 2u : 1u);
+  const uint32_t work = units * (elem == 2 ? 2u : 1u);
+  if (work > 12) return short_chunks;  // generator- or LDS-bound: full occupancy, short chunks
+  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), work <= 5 ? 1u : work <= 8 ? 3u : 4u};
+}
+
+// Dynamic LDS that, with `static_lds` bytes of the kernel's own, admits exactly `cap`
+// workgroups on a CU's 160 KiB (0: no cap).
+size_t occupancy_lds(uint32_t cap, size_t static_lds) {
+  if (cap == 0) return 0;
+  const size_t per_block = cap == 1 ? 96 * 1024 : cap == 2 ? 72 * 1024 : cap == 3 ? 48 * 1024 : 36 * 1024;
+  return per_block > static_lds ? per_block - static_lds : 0;
+}
+
+// Dynamic LDS above 64 KiB must be allowed per kernel before the launch.
+template <class K>
+void allow_lds(K kernel, size_t bytes) {
+  if (bytes > 65536)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              static_cast<int>(bytes));
+}
+
 template <class S, int N>
-void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, hipStream_t st) {
+void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, uint32_t cap, hipStream_t st) {
   const dim3 grid(plans_grid(ps)), block(kBlock);
   if (!w.update) {
+    const size_t pad = occupancy_lds(cap, 0);
+    auto go = [&](auto kernel, Probe b) {
+      allow_lds(kernel, pad);
+      kernel<<<grid, block, pad, st>>>(ps, gen, w.a, b);
+    };
     if (w.two)
-      perturb_kernel<S, true, N><<<grid, block, 0, st>>>(ps, gen, w.a, w.b);
+      go(perturb_kernel<S, true, N>, w.b);
     else
-      perturb_kernel<S, false, N><<<grid, block, 0, st>>>(ps, gen, w.a, w.a);
+      go(perturb_kernel<S, false, N>, w.a);
     return;
   }
   const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
-  const size_t lds = fixed ? 0 : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
+  const size_t table_bytes = static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
+  const size_t pad = occupancy_lds(cap, fixed ? table_bytes : 0);
+  const size_t tables = fixed ? 0 : table_bytes;
+  const size_t lds = tables > pad ? tables : pad;  // dynamic tables (up to 128 KiB) or the pad
   auto go = [&](auto kernel) {
-    if (lds > 65536)  // tables above 64 KiB: allow the workgroup the LDS it needs (<= 160 KiB)
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                static_cast<int>(lds));
+    allow_lds(kernel, lds);
     kernel<<<grid, block, lds, st>>>(ps, gen, w.k_base, w.K, w.n_groups, w.cf, w.lr, w.r);
   };
   if (w.restore) {
@@ -700,10 +828,12 @@ int make_update_sweep(Sweep& w, uint32_t k_base, uint32_t K, const float* c, flo
 // One contiguous tensor.
 template <class S>
 int run_one(void* params, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step, const Sweep& w, void* stream) {
+  const Shape sh = shape_for(n, sizeof(typename S::storage), w);
   Plans<1> ps{};
-  add_plan(ps, make_plan(params, offset, n, sizeof(typename S::storage), ChunkShape<S>::kElems));
+  ps.chunk_groups = sh.chunk_groups;
+  add_plan(ps, make_plan(params, offset, n, sizeof(typename S::storage), sh.chunk_groups));
   (void)hipGetLastError();
-  launch_sweep<S>(ps, make_gen(seed, step), w, static_cast<hipStream_t>(stream));
+  launch_sweep<S>(ps, make_gen(seed, step), w, sh.blocks_per_cu, static_cast<hipStream_t>(stream));
   return launch_status();
 }
 
@@ -746,20 +876,24 @@ int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_
                  void* stream) {
   const Gen gen = make_gen(seed, step);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  uint64_t total = 0;  // the call's weights decide the streaming shape of all its launches
+  for (uint32_t i = 0; i < n_segs; ++i) total += segs[i].n;
+  const Shape sh = shape_for(total, sizeof(typename S::storage), w);
   (void)hipGetLastError();
   Plans<kSegsPerLaunch> ps{};
+  ps.chunk_groups = sh.chunk_groups;
   for (uint32_t i = 0; i < n_segs; ++i) {
     if (segs[i].n == 0) continue;
     add_plan(ps, make_plan(segs[i].params, segs[i].offset, segs[i].n, sizeof(typename S::storage),
-                           ChunkShape<S>::kElems));
+                           sh.chunk_groups));
     if (ps.count == kSegsPerLaunch) {
-      launch_sweep<S>(ps, gen, w, st);
+      launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);
       if (launch_status() != ZO_OK) return ZO_ERR_HIP;
       ps.count = 0;
     }
   }
   if (ps.count) {
-    launch_sweep<S>(ps, gen, w, st);
+    launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);
     return launch_status();
   }
   return ZO_OK;
