@@ -274,6 +274,22 @@ struct Plans {
   Plan p[N];
 };
 
+// The first segment s in [from, count) with x < ends[s], where ends is nondecreasing and
+// x < ends[count - 1]: a binary search, so that finding a chunk's segment costs at most
+// log2(N) + 1 argument loads wherever the chunk lies.
+template <int N>
+__device__ __forceinline__ uint32_t segment_of(const uint64_t (&ends)[N], uint32_t from, uint32_t count, uint64_t x) {
+  uint32_t lo = from, hi = count - 1;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (x < ends[mid])
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  return lo;
+}
+
 template <class S>
 __device__ __forceinline__ void load_group(u32x4 (&d)[GroupShape<S>::kRows], const char* base, uint32_t lane) {
   const uint32_t v = vec_of_lane<S>(lane);
@@ -305,7 +321,7 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
   const uint64_t cg = ps.chunk_groups;
   uint32_t s = 0;
   for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + wave; c < total; c += n_waves) {
-    while (c >= ps.chunk_end[s]) ++s;
+    if (c >= ps.chunk_end[s]) s = segment_of(ps.chunk_end, s + 1, ps.count, c);
     const Plan& pl = ps.p[s];
     const uint64_t chunk = pl.c_first + (c - (s ? ps.chunk_end[s - 1] : 0));
     const uint64_t g0 = chunk * cg > pl.g_lo ? chunk * cg : pl.g_lo;
@@ -378,8 +394,7 @@ __device__ __forceinline__ void for_each_edge(const Plans<N>& ps, Body body) {
   const uint64_t n_edge = ps.edge_end[ps.count - 1];
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
   for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
-    uint32_t s = 0;
-    while (j >= ps.edge_end[s]) ++s;
+    const uint32_t s = segment_of(ps.edge_end, 0, ps.count, j);
     const Plan& pl = ps.p[s];
     const uint64_t lj = j - (s ? ps.edge_end[s - 1] : 0);
     body(pl, lj < pl.head_nt ? pl.head_t0 + lj : pl.tail_t0 + (lj - pl.head_nt));

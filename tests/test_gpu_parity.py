@@ -497,6 +497,49 @@ def test_segments_equal_flat_bits_for_update():
         np.testing.assert_array_equal(host_bits(t), flat_out[o:o + h.size])
 
 
+def test_segments_streaming_shape_equal_flat_bits():
+    """Above the 256 MiB streaming threshold: 56 separately allocated tensors of ragged sizes
+    (tiny ones among multi-million ones, none a multiple of the 32 KiB chunk, the first at a
+    global offset of 777) get, in every element, the bits that the single-buffer calls give
+    the same values laid out flat: perturb, a two-probe transition, the update with restore at
+    K = 16 (streaming shape) and the update at K = 64 (short chunks). The single-buffer calls
+    are themselves checked against the oracle at full size."""
+    rng = np.random.default_rng(13)
+    sizes = [int(x) for x in rng.integers(1, 8_000_000, 50)] + [1, 7, 1023, 1024, 1025, 16_385]
+    sizes = [sizes[i] for i in rng.permutation(len(sizes))]
+    total, base = sum(sizes), 777
+    assert 2 * total >= 256 << 20
+    note(f"segments at streaming scale: {len(sizes)} tensors, {total} weights")
+    flat = torch.empty(total, dtype=torch.bfloat16, device=DEV)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(14)
+    flat.normal_(0.0, 0.02, generator=gen)
+    starts = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64)
+    ts = [flat[int(a):int(a) + sz].clone() for a, sz in zip(starts, sizes)]
+    offs = [base + int(a) for a in starts]
+    seed, step, eps, lr = 31, 4, 1e-3, 1e-3
+    c16 = rng.standard_normal(16).astype(np.float32)
+    c64 = rng.standard_normal(64).astype(np.float32)
+
+    def same(what):
+        torch.cuda.synchronize()
+        for i, (t, a, sz) in enumerate(zip(ts, starts, sizes)):
+            assert torch.equal(t.view(torch.int16), flat[int(a):int(a) + sz].view(torch.int16)), f"{what}: tensor {i}"
+
+    zo.zo_perturb(flat, 3, eps, seed, step, offset=base)
+    zo.zo_perturb_segments(ts, offs, 3, eps, 0, 0.0, seed, step)
+    same("perturb")
+    zo.zo_perturb2(flat, 3, -2 * eps, 12, eps, seed, step, offset=base)
+    zo.zo_perturb_segments(ts, offs, 3, -2 * eps, 12, eps, seed, step)
+    same("perturb2")
+    zo.zo_update_restore(flat, c16, lr, seed, step, 12, -eps, offset=base)
+    zo.zo_update_segments(ts, offs, c16, lr, seed, step, 12, -eps)
+    same("update_restore K=16")
+    zo.zo_update_ex(flat, c64, lr, seed, step, offset=base)
+    zo.zo_update_segments(ts, offs, c64, lr, seed, step)
+    same("update K=64")
+
+
 def test_concurrent_streams_on_disjoint_tensors():
     """Calls on two streams over disjoint tensors run concurrently and give the serial results."""
     a_h = workloads.normal_bf16_bits(3_000_017, 20)
