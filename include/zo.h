@@ -48,13 +48,17 @@ typedef enum { ZO_F32 = 0, ZO_BF16 = 1 } zo_dtype;
 enum {
   ZO_OK = 0,
   ZO_ERR_NULL = -1,      /* a required pointer is NULL */
-  ZO_ERR_ARG = -2,       /* bad dtype, misalignment, K out of range, index overflow */
+  ZO_ERR_ARG = -2,       /* bad dtype, misalignment, K or n out of range, index overflow */
   ZO_ERR_NONFINITE = -3, /* a non-finite eps, lr, loss or coefficient */
   ZO_ERR_HIP = -4        /* the HIP runtime refused the launch */
 };
 
 /* Most probes one zo_update call applies (coefficients travel as kernel arguments, 4 KiB). */
 #define ZO_K_MAX 1024u
+
+/* Every call and every segment covers fewer than ZO_N_MAX = 2^40 elements (2 TiB of bf16,
+ * more than any one device holds); larger n is ZO_ERR_ARG. */
+#define ZO_N_MAX (1ull << 40)
 
 /* One tensor of a model's parameters, for the *_segments calls: `params` is caller-owned
  * device memory (aligned to the element size, on the device the stream belongs to) holding
@@ -72,7 +76,7 @@ typedef struct {
  * Arithmetic: one IEEE fp32 addition (bf16 weights widened exactly, the sum rounded back
  * to bf16 to nearest-even). The result is bit-exact and independent of launch shape.
  * Errors: ZO_ERR_NULL (params NULL with n > 0), ZO_ERR_ARG (dtype, alignment, index
- * overflow), ZO_ERR_NONFINITE (eps), ZO_ERR_HIP.
+ * overflow, n >= ZO_N_MAX), ZO_ERR_NONFINITE (eps), ZO_ERR_HIP.
  */
 int zo_perturb(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed,
                uint32_t step, uint32_t k, float eps, void* stream);
@@ -164,8 +168,8 @@ int zo_update_restore(void* params, zo_dtype dtype, uint64_t offset, uint64_t n,
  * segments' memory must not overlap. The tensors are swept in launches of up to 64
  * segments each (one sweep's worth of HBM traffic in total).
  * Errors: ZO_ERR_NULL (segs NULL with n_segs > 0, a segment's params NULL with n > 0),
- * ZO_ERR_ARG (dtype, a misaligned segment, an index range reaching 2^64, overlapping
- * segments), ZO_ERR_NONFINITE, all before anything is launched; ZO_ERR_HIP if a launch
+ * ZO_ERR_ARG (dtype, a misaligned segment, an index range reaching 2^64, a segment of
+ * ZO_N_MAX elements or more, overlapping segments), ZO_ERR_NONFINITE, all before anything is launched; ZO_ERR_HIP if a launch
  * fails, in which case earlier batches may already be enqueued.
  */
 int zo_perturb_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed,

@@ -33,6 +33,7 @@ LIB_PATH = os.path.join(PKG_DIR, "libzo.so")
 ZO_F32, ZO_BF16 = 0, 1
 ZO_OK, ZO_ERR_NULL, ZO_ERR_ARG, ZO_ERR_NONFINITE, ZO_ERR_HIP = 0, -1, -2, -3, -4
 ZO_K_MAX = 1024
+ZO_N_MAX = 1 << 40
 TILE = 16
 
 EXPORTS = ("zo_perturb", "zo_perturb2", "zo_probe_coeffs", "zo_probe_coeffs_ex", "zo_update", "zo_update_ex",

@@ -32,14 +32,18 @@ __global__ __launch_bounds__(kBlock) void xor_sweep(u32x4* p, uint64_t n_vecs, u
   if (key == 0 && n_vecs == 0) occupancy_pad[threadIdx.x] = 0;  // never taken (n_vecs > 0)
   const u32x4 k = {key, key, key, key};
   const uint32_t lane = threadIdx.x & 63u;
-  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * (kBlock / 64);
-  const uint64_t n_steps = n_vecs / kStepVecs;
-  const uint64_t n_chunks = (n_steps + kChunkSteps - 1) / kChunkSteps;
-  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * (kBlock / 64) + (threadIdx.x >> 6); c < n_chunks;
-       c += n_waves) {
-    const uint64_t s0 = c * kChunkSteps, s1 = s0 + kChunkSteps < n_steps ? s0 + kChunkSteps : n_steps;
-    u32x4* q = p + s0 * kStepVecs + lane;
-    // rotating register sets, the loads of the next two steps in flight (as the perturb sweep)
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t n_waves = gridDim.x * (kBlock / 64);
+  // 32-bit step and chunk indices (the host keeps a call below 2^31 chunks): the loop
+  // control stays on the scalar unit
+  const uint32_t n_steps = static_cast<uint32_t>(n_vecs / kStepVecs);
+  const uint32_t n_chunks = (n_steps + kChunkSteps - 1) / kChunkSteps;
+  for (uint32_t c = blockIdx.x * (kBlock / 64) + wave; c < n_chunks; c += n_waves) {
+    const uint32_t s0 = c * kChunkSteps, s1 = s0 + kChunkSteps < n_steps ? s0 + kChunkSteps : n_steps;
+    u32x4* q = p + static_cast<uint64_t>(s0) * kStepVecs + lane;
+    // rotating register sets with the loads of the next two steps in flight, and one full
+    // step run before the loop so that the loop is entered with the same memory operations
+    // outstanding as on its back edge (as the perturb sweep)
     u32x4 x[2], y[2], z[2];
     auto prefetch2 = [&](u32x4 (&d)[2]) {
       load_step(d, q + 2 * kStepVecs);
@@ -49,49 +53,64 @@ __global__ __launch_bounds__(kBlock) void xor_sweep(u32x4* p, uint64_t n_vecs, u
       store_step(q, d, k);
       q += kStepVecs;
     };
-    load_step(x, q);
-    uint64_t s = s0;
-    if (s + 1 < s1) load_step(y, q + kStepVecs);
-    for (; s + 4 < s1; s += 3) {
+    auto step3 = [&]() {
       prefetch2(z);
       work(x);
       prefetch2(x);
       work(y);
       prefetch2(y);
       work(z);
-    }
-    const uint64_t left = s1 - s;  // 1 to 4
-    if (left >= 3) {
-      prefetch2(z);
-      work(x);
-      if (left == 4) {
-        prefetch2(x);
-        work(y);
-        work(z);
+    };
+    auto last = [&](uint32_t left) {  // 2 to 4 steps left, x and y requested
+      if (left >= 3) {
+        prefetch2(z);
         work(x);
+        if (left == 4) {
+          prefetch2(x);
+          work(y);
+          work(z);
+          work(x);
+        } else {
+          work(y);
+          work(z);
+        }
       } else {
+        work(x);
         work(y);
-        work(z);
       }
+    };
+    load_step(x, q);
+    uint32_t s = s0;
+    if (s + 4 < s1) {
+      load_step(y, q + kStepVecs);
+      step3();
+      s += 3;
+      for (; s + 4 < s1; s += 3) step3();
+      last(s1 - s);
+    } else if (s + 1 < s1) {
+      load_step(y, q + kStepVecs);
+      last(s1 - s);
     } else {
       work(x);
-      if (left == 2) work(y);
     }
   }
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t v = n_steps * kStepVecs + static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; v < n_vecs;
-       v += stride)
+  for (uint64_t v = static_cast<uint64_t>(n_steps) * kStepVecs + static_cast<uint64_t>(blockIdx.x) * kBlock +
+                    threadIdx.x;
+       v < n_vecs; v += stride)
     p[v] = p[v] ^ k;
 }
 
 }  // namespace
 
-// 0 on success; -1 for a null pointer with bytes > 0; -2 when p is not 16-byte aligned or
-// bytes is not a multiple of 16; -4 when the launch fails. Asynchronous on `stream`.
+// 0 on success; -1 for a null pointer with bytes > 0; -2 when p is not 16-byte aligned,
+// bytes is not a multiple of 16 or reaches 2^46; -4 when the launch fails. Asynchronous on
+// `stream`.
 extern "C" int zo_calib_rmw(void* p, uint64_t bytes, uint32_t key, void* stream) {
   if (bytes == 0) return 0;
   if (p == nullptr) return -1;
   if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0 || (bytes & 15u) != 0) return -2;
+  if (bytes >= (1ull << 46)) return -2;  // 2^31 chunks of 32 KiB
   const uint64_t n_vecs = bytes / 16;
   const uint64_t chunks = (n_vecs / kStepVecs + kChunkSteps - 1) / kChunkSteps;
   uint64_t blocks = (chunks + 3) / 4;

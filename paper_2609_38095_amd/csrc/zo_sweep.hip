@@ -48,6 +48,9 @@ namespace {
 constexpr uint32_t kTile = 16;    // elements per generator block
 constexpr uint32_t kBlock = 256;  // threads per workgroup (4 waves)
 constexpr uint32_t kWavesPerBlock = kBlock / 64;
+// s_waitcnt immediate for vmcnt(2) that leaves expcnt and lgkmcnt unconstrained (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+constexpr int kWaitVmcnt2 = 0x0F72;
 constexpr uint64_t kGroupElems = 1024;      // elements per row group (one Philox block per lane)
 constexpr uint64_t kMaxChunkBytes = 32768;  // bytes a wave streams per chunk, at most
 constexpr uint32_t kDefaultMaxBlocks = 65536;
@@ -251,16 +254,22 @@ __device__ __forceinline__ void tile_elementwise(typename S::storage* params, ui
 }
 
 // One segment: global elements [lo, hi) stored from `base` (the address of global element lo).
-// The full row groups [g_lo, g_hi) (global group indices) take the vector path, in chunks of
-// up to `chunk_groups` groups aligned to multiples of chunk_groups: chunks
-// [c_first, c_first + n_chunks) meet the range. The edge tiles [head_t0, +head_nt) and
-// [tail_t0, +tail_nt) (fewer than 1024 elements at each end) take the element-wise path.
+// The `span` full row groups from global group g_lo (stored from `gbase`) take the vector
+// path, in chunks of up to `chunk_groups` groups aligned to multiples of chunk_groups in the
+// global group index: the segment's first chunk starts `head` = g_lo mod chunk_groups groups
+// before g_lo. The edge tiles [head_t0, +head_nt) and [tail_t0, +tail_nt) (fewer than 1024
+// elements at each end) take the element-wise path. The kernels walk chunks and groups with
+// 32-bit indices relative to the segment (compares of 64-bit indices need a vector register
+// on gfx950, and writing one that a pending store still reads makes the wave wait for that
+// store); the host keeps a segment below 2^30 row groups and a launch below 2^31 chunks.
 struct Plan {
   char* base;
   uint64_t lo, hi;
-  uint64_t g_lo, g_hi;
-  uint64_t c_first, n_chunks;
-  uint64_t head_t0, head_nt, tail_t0, tail_nt;
+  char* gbase;
+  uint64_t g_lo;
+  uint32_t head, span;
+  uint64_t head_t0, tail_t0;
+  uint32_t head_nt, tail_nt;
 };
 
 // The segments one launch covers. Their chunks and edge tiles are numbered consecutively:
@@ -269,8 +278,8 @@ template <int N>
 struct Plans {
   uint32_t count;
   uint32_t chunk_groups;
-  uint64_t chunk_end[N];
-  uint64_t edge_end[N];
+  uint32_t chunk_end[N];
+  uint32_t edge_end[N];
   Plan p[N];
 };
 
@@ -278,7 +287,7 @@ struct Plans {
 // x < ends[count - 1]: a binary search, so that finding a chunk's segment costs at most
 // log2(N) + 1 argument loads wherever the chunk lies.
 template <int N>
-__device__ __forceinline__ uint32_t segment_of(const uint64_t (&ends)[N], uint32_t from, uint32_t count, uint64_t x) {
+__device__ __forceinline__ uint32_t segment_of(const uint32_t (&ends)[N], uint32_t from, uint32_t count, uint32_t x) {
   uint32_t lo = from, hi = count - 1;
   while (lo < hi) {
     const uint32_t mid = (lo + hi) >> 1;
@@ -308,47 +317,65 @@ __device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupSh
 // group's global vector index and d its data, and stores what the body leaves in d. One
 // wave per chunk walks the chunk's groups in address order with the loads of the next AHEAD
 // groups in flight while the body works on the current one (each wave streams up to 32 KiB,
-// reads and writes interleaved; two ahead pays for the light perturb, one for the update). A
-// wave's chunk indices increase, so its segment cursor only moves forward.
-template <class S, int AHEAD, int N, class Body>
+// reads and writes interleaved). A wave's chunk indices increase, so its segment cursor
+// only moves forward. PACED (two ahead only): each step of three groups first waits until
+// its newest prefetch is all the wave has outstanding, earlier stores included. The
+// lightest sweeps stream HBM faster paced (the one-probe bf16 perturb: 6.57 TB/s against
+// 6.40 with every request the loop allows in flight), heavier ones need the overlap.
+template <class S, int AHEAD, int N, bool PACED = false, class Body>
 __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
+  static_assert(!PACED || AHEAD == 2, "pacing applies to the two-ahead loop");
   static_assert(AHEAD == 1 || AHEAD == 2, "one or two groups in flight");
   using G = GroupShape<S>;
-  const uint64_t n_waves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
-  const uint64_t total = ps.chunk_end[ps.count - 1];
+  const uint32_t n_waves = gridDim.x * kWavesPerBlock;
+  const uint32_t total = ps.chunk_end[ps.count - 1];
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t lane = threadIdx.x & 63u;
-  const uint64_t cg = ps.chunk_groups;
+  const uint32_t cg = ps.chunk_groups;
   uint32_t s = 0;
-  for (uint64_t c = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + wave; c < total; c += n_waves) {
+  for (uint32_t c = blockIdx.x * kWavesPerBlock + wave; c < total; c += n_waves) {
     if (c >= ps.chunk_end[s]) s = segment_of(ps.chunk_end, s + 1, ps.count, c);
     const Plan& pl = ps.p[s];
-    const uint64_t chunk = pl.c_first + (c - (s ? ps.chunk_end[s - 1] : 0));
-    const uint64_t g0 = chunk * cg > pl.g_lo ? chunk * cg : pl.g_lo;
-    const uint64_t g1 = chunk * cg + cg < pl.g_hi ? chunk * cg + cg : pl.g_hi;
-    char* base = pl.base + (g0 * kGroupElems - pl.lo) * sizeof(typename S::storage);
+    // the chunk's groups [g0, g1), relative to the segment's first full group (a select on the
+    // chunk index, not a clamped subtraction, which has no scalar form)
+    const uint32_t j = c - (s ? ps.chunk_end[s - 1] : 0);
+    const uint32_t end = (j + 1) * cg - pl.head;
+    const uint32_t g0 = j ? j * cg - pl.head : 0u;
+    const uint32_t g1 = end < pl.span ? end : pl.span;
+    const uint64_t g_base = pl.g_lo;
+    char* base = pl.gbase + static_cast<uint64_t>(g0) * G::kBytes;
     // Rotating register sets: while the body works on one group, the loads of the next AHEAD
     // groups are in flight. No register of an outstanding load is ever copied, and inside the
     // loops the prefetches do not depend on a branch (either would make the compiler wait
     // for every outstanding load before the work).
     u32x4 x[G::kRows], y[G::kRows], z[G::kRows];
-    auto work = [&](u32x4 (&cur)[G::kRows], uint64_t g) {
-      body(g * G::kVecs, cur, lane);
+    auto work = [&](u32x4 (&cur)[G::kRows], uint32_t g) {
+      body((g_base + g) * G::kVecs, cur, lane);
       store_group<S>(base, cur, lane);
       base += G::kBytes;
     };
-    auto prefetch = [&](u32x4 (&nxt)[G::kRows], uint64_t ahead) {
+    auto prefetch = [&](u32x4 (&nxt)[G::kRows], uint32_t ahead) {
       load_group<S>(nxt, base + ahead * G::kBytes, lane);
       __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the work (the scheduler sinks it)
     };
     load_group<S>(x, base, lane);
-    uint64_t g = g0;
+    uint32_t g = g0;
+    // Each steady-state loop is entered only after one full step of it has run (peeled), so
+    // that the loop is entered with the same loads and stores outstanding as its back edge:
+    // the compiler then waits for exactly the group a step needs. Entered straight from the
+    // first loads, it would merge the two states and wait, in every step, until only the
+    // newest loads were outstanding (previous stores and later prefetches included).
     if constexpr (AHEAD == 1) {
-      for (; g + 2 < g1; g += 2) {  // at least three groups left: two steps that both prefetch
+      auto step2 = [&]() {
         prefetch(y, 1);
         work(x, g);
         prefetch(x, 1);
         work(y, g + 1);
+        g += 2;
+      };
+      if (g + 2 < g1) {  // at least three groups left: steps of two that both prefetch
+        step2();
+        while (g + 2 < g1) step2();
       }
       if (g + 1 < g1) {  // two groups left
         prefetch(y, 1);
@@ -358,31 +385,45 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
         work(x, g);
       }
     } else {
-      if (g + 1 < g1) load_group<S>(y, base + G::kBytes, lane);
-      for (; g + 4 < g1; g += 3) {  // at least five groups left: three steps that prefetch two ahead
+      auto step3 = [&]() {
         prefetch(z, 2);
+        if constexpr (PACED) __builtin_amdgcn_s_waitcnt(kWaitVmcnt2);  // only z's loads stay in flight
         work(x, g);
         prefetch(x, 2);
         work(y, g + 1);
         prefetch(y, 2);
         work(z, g + 2);
-      }
-      const uint64_t left = g1 - g;  // 1 to 4; x (and y when left > 1) requested
-      if (left >= 3) {
-        prefetch(z, 2);
-        work(x, g);
-        if (left == 4) {
-          prefetch(x, 2);
-          work(y, g + 1);
-          work(z, g + 2);
-          work(x, g + 3);
+        g += 3;
+      };
+      // 2 to 4 groups left, x and y requested
+      auto last = [&]() {
+        if (g + 2 < g1) {
+          prefetch(z, 2);
+          work(x, g);
+          if (g + 3 < g1) {
+            prefetch(x, 2);
+            work(y, g + 1);
+            work(z, g + 2);
+            work(x, g + 3);
+          } else {
+            work(y, g + 1);
+            work(z, g + 2);
+          }
         } else {
+          work(x, g);
           work(y, g + 1);
-          work(z, g + 2);
         }
+      };
+      if (g + 4 < g1) {  // at least five groups left: steps of three that prefetch two ahead
+        load_group<S>(y, base + G::kBytes, lane);
+        step3();
+        while (g + 4 < g1) step3();
+        last();
+      } else if (g + 1 < g1) {
+        load_group<S>(y, base + G::kBytes, lane);
+        last();
       } else {
         work(x, g);
-        if (left == 2) work(y, g + 1);
       }
     }
   }
@@ -391,12 +432,12 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
 // Calls body(plan, tile) for every edge tile of the launch, one lane per tile.
 template <int N, class Body>
 __device__ __forceinline__ void for_each_edge(const Plans<N>& ps, Body body) {
-  const uint64_t n_edge = ps.edge_end[ps.count - 1];
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t j = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n_edge; j += stride) {
+  const uint32_t n_edge = ps.edge_end[ps.count - 1];
+  const uint32_t stride = gridDim.x * kBlock;
+  for (uint32_t j = blockIdx.x * kBlock + threadIdx.x; j < n_edge; j += stride) {
     const uint32_t s = segment_of(ps.edge_end, 0, ps.count, j);
     const Plan& pl = ps.p[s];
-    const uint64_t lj = j - (s ? ps.edge_end[s - 1] : 0);
+    const uint32_t lj = j - (s ? ps.edge_end[s - 1] : 0);
     body(pl, lj < pl.head_nt ? pl.head_t0 + lj : pl.tail_t0 + (lj - pl.head_nt));
   }
 }
@@ -410,13 +451,13 @@ struct Probe {
   __device__ __forceinline__ float delta(uint32_t byte) const { return ((byte >> bit) & 1u) ? eps : -eps; }
 };
 
-template <class S, bool TWO, int N>
+template <class S, bool TWO, int N, bool PACED>
 __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, Probe a, Probe b) {
   extern __shared__ uint32_t occupancy_pad[];  // dynamic LDS only limits workgroups per CU
   if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count <= 64)
   constexpr int R = GroupShape<S>::kRows;
   const bool shared_group = a.group == b.group;
-  for_each_group<S, 2>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+  for_each_group<S, 2, N, PACED>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     uint32_t Wa[R][S::kWords], Wb[R][S::kWords];
     group_words(gen, vbase, lane, a.group, Wa, S());
     if (TWO) {
@@ -589,7 +630,10 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
   build_tables(tab, cf, k_base, K, n_groups);
   const uint32_t g_first = k_base / 8;
   constexpr int R = GroupShape<S>::kRows;
-  for_each_group<S, 1>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+  // two groups in flight for the table counts that stream at one or two workgroups per CU;
+  // one for the heavier updates, which run more waves per CU
+  constexpr int kAhead = NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
+  for_each_group<S, kAhead, N>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
     group_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
     uint32_t Wr[R][S::kWords];  // the restore probe's generator words
@@ -630,7 +674,8 @@ __global__ __launch_bounds__(kBlock) void gen_bits_kernel(uint8_t* out, uint64_t
 
 // ---------------------------------------------------------------------------------------
 // Host side.
-constexpr int kSegsPerLaunch = 64;  // segments per batched launch (kernel arguments, ~5.6 KiB)
+constexpr int kSegsPerLaunch = 64;                 // segments per batched launch (kernel arguments, ~5 KiB)
+constexpr uint64_t kMaxLaunchChunks = 1ull << 31;  // chunks per launch: 32-bit indices with room for the stride
 
 uint32_t cap_blocks() { return g_max_blocks ? g_max_blocks : kDefaultMaxBlocks; }
 
@@ -647,6 +692,7 @@ int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n) {
   if (params == nullptr) return ZO_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(params) % (dt == ZO_F32 ? 4 : 2) != 0) return ZO_ERR_ARG;
   if (offset + n < offset || offset + n == 0) return ZO_ERR_ARG;  // reaches 2^64
+  if (n >= ZO_N_MAX) return ZO_ERR_ARG;  // more weights than a device holds
   return ZO_OK;
 }
 
@@ -654,7 +700,7 @@ uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
 
 // Full row groups need the address of global element 0 (params shifted back by offset
 // elements) to be 16-byte aligned, so that every group vector is an aligned 16 bytes.
-Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t chunk_groups) {
+Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint32_t chunk_groups) {
   Plan pl{};
   pl.base = static_cast<char*>(params);
   pl.lo = offset;
@@ -664,37 +710,42 @@ Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint64_t 
   uint64_t head_end = pl.hi, tail_begin = pl.hi;
   if ((base & 15u) == 0) {
     const uint64_t g_lo = ceil_div(pl.lo, kGroupElems), g_hi = pl.hi / kGroupElems;
-    if (g_lo < g_hi) {
+    if (g_lo < g_hi) {  // g_hi - g_lo < 2^30: n < ZO_N_MAX is checked first
       pl.g_lo = g_lo;
-      pl.g_hi = g_hi;
-      pl.c_first = g_lo / chunk_groups;
-      pl.n_chunks = ceil_div(g_hi, chunk_groups) - pl.c_first;
+      pl.span = static_cast<uint32_t>(g_hi - g_lo);
+      pl.head = static_cast<uint32_t>(g_lo % chunk_groups);
+      pl.gbase = pl.base + (g_lo * kGroupElems - pl.lo) * elem;
       head_end = g_lo * kGroupElems;
       tail_begin = g_hi * kGroupElems;
     }
   }
   if (head_end > pl.lo) {
     pl.head_t0 = pl.lo / kTile;
-    pl.head_nt = ceil_div(head_end, kTile) - pl.head_t0;
+    pl.head_nt = static_cast<uint32_t>(ceil_div(head_end, kTile) - pl.head_t0);
   }
   if (pl.hi > tail_begin) {
     pl.tail_t0 = tail_begin / kTile;
-    pl.tail_nt = ceil_div(pl.hi, kTile) - pl.tail_t0;
+    pl.tail_nt = static_cast<uint32_t>(ceil_div(pl.hi, kTile) - pl.tail_t0);
   }
   return pl;
+}
+
+// Chunks that meet a plan's full row groups (fewer than 2^30 + 2).
+uint32_t plan_chunks(const Plan& pl, uint32_t chunk_groups) {
+  return pl.span ? static_cast<uint32_t>(ceil_div(static_cast<uint64_t>(pl.head) + pl.span, chunk_groups)) : 0u;
 }
 
 template <int N>
 void add_plan(Plans<N>& ps, const Plan& pl) {
   const uint32_t s = ps.count++;
   ps.p[s] = pl;
-  ps.chunk_end[s] = (s ? ps.chunk_end[s - 1] : 0) + pl.n_chunks;
+  ps.chunk_end[s] = (s ? ps.chunk_end[s - 1] : 0) + plan_chunks(pl, ps.chunk_groups);
   ps.edge_end[s] = (s ? ps.edge_end[s - 1] : 0) + pl.head_nt + pl.tail_nt;
 }
 
 template <int N>
 uint32_t plans_grid(const Plans<N>& ps) {
-  const uint64_t chunks = ps.chunk_end[ps.count - 1], edges = ps.edge_end[ps.count - 1];
+  const uint32_t chunks = ps.chunk_end[ps.count - 1], edges = ps.edge_end[ps.count - 1];
   const uint32_t a = chunks ? grid_for(chunks, kWavesPerBlock) : 1;
   const uint32_t b = grid_for(edges, kBlock);
   return a > b ? a : b;
@@ -722,16 +773,16 @@ struct Sweep {
 
 // Streaming shape of a launch over `elements` weights of `elem` bytes. HBM sustains these
 // in-place sweeps best as few long sequential read-write streams: each wave walks up to
-// kMaxChunkBytes of consecutive row groups with the next group in flight, and occupancy is
-// capped so that few waves stream at once (measured on one buffer: 6.2 TB/s for the bf16
-// perturb at one workgroup per CU against 5.4 at full occupancy). The cap rises with the
-// generator work per byte, which a wave must hide behind its own loads: work = generator
-// blocks per row group, an update's probe group counting twice (block and table lookups),
-// doubled for bf16 (twice the elements per byte). Sweeps smaller than the 256 MiB Infinity
-// Cache keep 4 KiB chunks at full occupancy. Thresholds from measured sweeps of every kernel
-// over occupancy on OPT-1.3B and OPT-13B shaped bf16 and 3 G-element fp32 buffers; kernels
-// with more work (K >= 32 updates in bf16, K >= 48 in fp32) are bound by the generator or the
-// LDS and keep 4 KiB chunks at full occupancy.
+// kMaxChunkBytes of consecutive row groups with the next one or two groups in flight, and
+// occupancy is capped with dynamic LDS so that few waves stream at once (the bf16 perturb on
+// an OPT-13B shaped buffer: 6.5 TB/s at one workgroup per CU, 5.6 at full occupancy). An
+// update needs more waves where its generator and table work per byte outgrows what one wave
+// overlaps with its own loads; the caps below are the fastest of 1-4 workgroups per CU and
+// full occupancy, 16 to 64 KiB chunks and one or two groups in flight, measured for every
+// kernel on OPT-13B shaped bf16 and 3 G-element fp32 buffers. Updates with more probe groups
+// (K >= 32 in bf16, K >= 56 in fp32) are bound by the generator or the LDS table lookups
+// and keep 4 KiB chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity
+// Cache.
 struct Shape {
   uint32_t chunk_groups;
   uint32_t blocks_per_cu;  // 0: no cap
@@ -743,10 +794,16 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   const uint64_t group_bytes = kGroupElems * elem;
   const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0};
   if (elements * elem < kStreamBytes) return short_chunks;
-  const uint32_t units = w.update ? 2 * w.n_groups + (w.restore ? 1u : 0u) : (w.two && w.a.group != w.b.group ? 2u : 1u);
-  const uint32_t work = units * (elem == 2 ? 2u : 1u);
-  if (work > 12) return short_chunks;  // generator- or LDS-bound: full occupancy, short chunks
-  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), work <= 5 ? 1u : work <= 8 ? 3u : 4u};
+  uint32_t cap = 1;  // the perturb kernels, one or two probes
+  if (w.update) {
+    const uint32_t g = w.n_groups;
+    if (elem == 2)
+      cap = g == 1 ? 1 : g == 2 ? (w.restore ? 2 : 1) : g == 3 ? 3 : 0;
+    else
+      cap = g <= 3 ? 1 : g == 4 ? 2 : g <= 6 ? 3 : 0;
+  }
+  if (cap == 0) return short_chunks;
+  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap};
 }
 
 // Dynamic LDS that, with `static_lds` bytes of the kernel's own, admits exactly `cap`
@@ -774,10 +831,13 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, uint32_t c
       allow_lds(kernel, pad);
       kernel<<<grid, block, pad, st>>>(ps, gen, w.a, b);
     };
+    // paced when the generator work per byte is lightest: one probe group, or fp32 with two
+    const bool two_groups = w.two && w.a.group != w.b.group;
+    const bool paced = (two_groups ? 2u : 1u) * (sizeof(typename S::storage) == 2 ? 2u : 1u) <= 2u;
     if (w.two)
-      go(perturb_kernel<S, true, N>, w.b);
+      paced ? go(perturb_kernel<S, true, N, true>, w.b) : go(perturb_kernel<S, true, N, false>, w.b);
     else
-      go(perturb_kernel<S, false, N>, w.a);
+      paced ? go(perturb_kernel<S, false, N, true>, w.a) : go(perturb_kernel<S, false, N, false>, w.a);
     return;
   }
   const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
@@ -899,8 +959,13 @@ int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_
   ps.chunk_groups = sh.chunk_groups;
   for (uint32_t i = 0; i < n_segs; ++i) {
     if (segs[i].n == 0) continue;
-    add_plan(ps, make_plan(segs[i].params, segs[i].offset, segs[i].n, sizeof(typename S::storage),
-                           sh.chunk_groups));
+    const Plan pl = make_plan(segs[i].params, segs[i].offset, segs[i].n, sizeof(typename S::storage), sh.chunk_groups);
+    if (ps.count && ps.chunk_end[ps.count - 1] + static_cast<uint64_t>(plan_chunks(pl, sh.chunk_groups)) >= kMaxLaunchChunks) {
+      launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);  // keep a launch's chunk count 32-bit
+      if (launch_status() != ZO_OK) return ZO_ERR_HIP;
+      ps.count = 0;
+    }
+    add_plan(ps, pl);
     if (ps.count == kSegsPerLaunch) {
       launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);
       if (launch_status() != ZO_OK) return ZO_ERR_HIP;

@@ -61,6 +61,7 @@ def test_calibration_library_exports_its_header():
 def test_header_constants_match_binding():
     text = open(os.path.join(ROOT, "include", "zo.h")).read()
     assert int(re.search(r"#define ZO_K_MAX (\d+)u", text).group(1)) == zo.ZO_K_MAX
+    assert 1 << int(re.search(r"#define ZO_N_MAX \(1ull << (\d+)\)", text).group(1)) == zo.ZO_N_MAX
     for name, val in [("ZO_ERR_NULL", zo.ZO_ERR_NULL), ("ZO_ERR_ARG", zo.ZO_ERR_ARG),
                       ("ZO_ERR_NONFINITE", zo.ZO_ERR_NONFINITE), ("ZO_ERR_HIP", zo.ZO_ERR_HIP)]:
         assert int(re.search(name + r"\s*=\s*(-?\d+)", text).group(1)) == val
@@ -133,6 +134,8 @@ def test_sweep_validation_returns_before_launch(lib):
     assert lib.zo_perturb(odd, zo.ZO_F32, 0, 10, 0, 0, 0, 1e-3, None) == zo.ZO_ERR_ARG
     assert lib.zo_perturb(odd, zo.ZO_BF16, 0, 10, 0, 0, 0, 1e-3, None) == zo.ZO_ERR_ARG
     assert lib.zo_perturb(fake, zo.ZO_F32, 2 ** 64 - 5, 10, 0, 0, 0, 1e-3, None) == zo.ZO_ERR_ARG
+    assert lib.zo_perturb(fake, zo.ZO_BF16, 0, zo.ZO_N_MAX, 0, 0, 0, 1e-3, None) == zo.ZO_ERR_ARG
+    assert lib.zo_update(fake, zo.ZO_BF16, zo.ZO_N_MAX, 0, 0, 1, c1, 1e-3, None) == zo.ZO_ERR_ARG
     assert lib.zo_perturb(fake, zo.ZO_F32, 0, 10, 0, 0, 0, float("inf"), None) == zo.ZO_ERR_NONFINITE
     assert lib.zo_perturb(None, zo.ZO_F32, 0, 0, 0, 0, 0, 1e-3, None) == zo.ZO_OK  # n = 0: no-op
     assert lib.zo_update(fake, zo.ZO_F32, 10, 0, 0, zo.ZO_K_MAX + 1, big, 1e-3, None) == zo.ZO_ERR_ARG
@@ -163,6 +166,8 @@ def test_segments_validation_returns_before_launch(lib):
     assert lib.zo_perturb_segments(arr((None, 0, 5)), 1, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_NULL
     assert lib.zo_perturb_segments(arr((0x10002, 0, 5)), 1, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
     assert lib.zo_perturb_segments(arr((0x10000, 2 ** 64 - 2, 5)), 1, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
+    too_big = arr((0x10000, 0, 100), (0x20000, 100, zo.ZO_N_MAX))
+    assert lib.zo_perturb_segments(too_big, 2, zo.ZO_BF16, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
     # overlapping memory (the second starts inside the first)
     overl = arr((0x10000, 0, 100), (0x10000 + 4 * 99, 100, 10))
     assert lib.zo_perturb_segments(overl, 2, zo.ZO_F32, 0, 0, 0, 1e-3, 1, 1e-3, None) == zo.ZO_ERR_ARG
