@@ -38,6 +38,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -322,8 +323,11 @@ __device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupSh
 // its newest prefetch is all the wave has outstanding, earlier stores included. The
 // lightest sweeps stream HBM faster paced (the one-probe bf16 perturb: 6.57 TB/s against
 // 6.40 with every request the loop allows in flight), heavier ones need the overlap.
-template <class S, int AHEAD, int N, bool PACED = false, class Body>
-__device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
+// prologue() runs once per wave, after the loads of the wave's first group are issued (at
+// once for a wave without chunks), so that work such as building the update's LDS tables
+// overlaps their latency; it may hold a workgroup barrier, which every wave reaches once.
+template <class S, int AHEAD, int N, bool PACED = false, class Body, class Prologue>
+__device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Prologue prologue) {
   static_assert(!PACED || AHEAD == 2, "pacing applies to the two-ahead loop");
   static_assert(AHEAD == 1 || AHEAD == 2, "one or two groups in flight");
   using G = GroupShape<S>;
@@ -333,7 +337,9 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t cg = ps.chunk_groups;
   uint32_t s = 0;
-  for (uint32_t c = blockIdx.x * kWavesPerBlock + wave; c < total; c += n_waves) {
+  uint32_t c = blockIdx.x * kWavesPerBlock + wave;
+  if (c >= total) prologue();
+  for (bool first = true; c < total; c += n_waves, first = false) {
     if (c >= ps.chunk_end[s]) s = segment_of(ps.chunk_end, s + 1, ps.count, c);
     const Plan& pl = ps.p[s];
     // the chunk's groups [g0, g1), relative to the segment's first full group (a select on the
@@ -359,6 +365,7 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body) {
       __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the work (the scheduler sinks it)
     };
     load_group<S>(x, base, lane);
+    if (first) prologue();
     uint32_t g = g0;
     // Each steady-state loop is entered only after one full step of it has run (peeled), so
     // that the loop is entered with the same loads and stores outstanding as its back edge:
@@ -457,6 +464,7 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
   if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count <= 64)
   constexpr int R = GroupShape<S>::kRows;
   const bool shared_group = a.group == b.group;
+  auto no_prologue = []() {};
   for_each_group<S, 2, N, PACED>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     uint32_t Wa[R][S::kWords], Wb[R][S::kWords];
     group_words(gen, vbase, lane, a.group, Wa, S());
@@ -482,7 +490,7 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
       }
       d[u] = S::pack(v);
     }
-  });
+  }, no_prologue);
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     const uint4 ra = gen.block(t, a.group);
     const uint4 rb = TWO ? gen.block(t, b.group) : ra;
@@ -501,11 +509,22 @@ struct Coefs {
   float c[ZO_K_MAX];
 };
 
-// Build the n_groups x 256 table in LDS. Entry (g, b): sum over the group's 8 probe slots
-// of +-c (bit set: +c); slots outside [k_base, k_base + K) contribute 0; pairwise. Thread b
-// writes entry b of every group: the group loop and the coefficient reads are uniform (scalar
-// loads), and the sign of slot s is an XOR of the coefficient's sign bit with bit s of ~b.
+// Spread tables, for one or two probe groups in streaming launches: 32 copies of each
+// 256-entry table, interleaved so that copy r of entry e of group g is float 64 e + 32 g + r.
+// Lane l reads copy l mod 32, which sits in LDS bank l mod 32, so a 64-lane read of random
+// bytes takes 2 LDS cycles instead of about 6.3 when all lanes share one copy. A lookup's
+// byte address, 256 e + 4 (l mod 32) + 128 g, is one byte permute of the generator word and
+// the lane's copy offset (as many instructions as a lookup into a shared table). 64 KiB per
+// workgroup.
+constexpr uint32_t kSpreadFloats = 256 * 64;
+
+// Build the n_groups x 256 table in LDS (SPREAD: the 32 interleaved copies). Entry (g, b):
+// sum over the group's 8 probe slots of +-c (bit set: +c); slots outside [k_base, k_base + K)
+// contribute 0; pairwise. Thread b writes entry b of every group: the group loop and the
+// coefficient reads are uniform (scalar loads), and the sign of slot s is an XOR of the
+// coefficient's sign bit with bit s of ~b.
 static_assert(kBlock == 256, "one table entry per thread");
+template <bool SPREAD>
 __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
                                              uint32_t n_groups) {
   const uint32_t b = threadIdx.x;
@@ -521,16 +540,31 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
       const float cv = (k >= k_base && k - k_base < K) ? cf.c[k - k_base] : 0.0f;
       v[s] = __uint_as_float(__float_as_uint(cv) ^ flip[s]);
     }
-    tab[256u * g + b] = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+    const float t = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+    if constexpr (SPREAD) {
+      const float4 t4 = make_float4(t, t, t, t);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) *reinterpret_cast<float4*>(tab + 64u * b + 32u * g + 4u * q) = t4;
+    } else {
+      tab[256u * g + b] = t;
+    }
   }
   __syncthreads();
 }
 
+// Spread-table lookup: one byte permute forms the address (byte 0: the lane's copy offset
+// `lane_off`, byte 1: byte e of w, upper bytes 0), then the float there plus the group's
+// 128-byte offset.
+__device__ __forceinline__ float spread_at(const float* tab, uint32_t lane_off, uint32_t w, int e, uint32_t g) {
+  const uint32_t addr = __builtin_amdgcn_perm(w, lane_off, 0x0C0C0000u | ((4u + static_cast<uint32_t>(e)) << 8));
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + addr + 128u * g);
+}
+
 // acc[u][e] (+)= table value of probe group g for each element of the row group.
-template <class S, bool FIRST>
+template <class S, bool FIRST, bool SPREAD>
 __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                           const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t g,
-                                          uint32_t g_first) {
+                                          uint32_t g_first, uint32_t lane_off) {
   constexpr int R = GroupShape<S>::kRows;
   uint32_t W[R][S::kWords];
   group_words(gen, vbase, lane, g_first + g, W, S());
@@ -539,29 +573,35 @@ __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::
   for (int u = 0; u < R; ++u)
 #pragma unroll
     for (int e = 0; e < S::kVecElems; ++e) {
-      const float x = table_at(tg, W[u][e >> 2], e & 3);
+      float x;
+      if constexpr (SPREAD)
+        x = spread_at(tab, lane_off, W[u][e >> 2], e & 3, g);
+      else
+        x = table_at(tg, W[u][e >> 2], e & 3);
       acc[u][e] = FIRST ? x : acc[u][e] + x;
     }
 }
 
 // Sum of the tables of probe groups 0 .. n_groups-1 for the row group: NG > 0 fixes the count
 // at compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
-template <class S, int NG>
+template <class S, int NG, bool SPREAD>
 __device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                            const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t n_groups,
-                                           uint32_t g_first) {
+                                           uint32_t g_first, uint32_t lane_off) {
   constexpr int R = GroupShape<S>::kRows;
+  static_assert(!SPREAD || NG == 1 || NG == 2, "spread tables hold one or two groups");
   if constexpr (NG > 0) {
-    add_group<S, true>(acc, tab, gen, vbase, lane, 0, g_first);
+    add_group<S, true, SPREAD>(acc, tab, gen, vbase, lane, 0, g_first, lane_off);
 #pragma unroll
-    for (int g = 1; g < NG; ++g) add_group<S, false>(acc, tab, gen, vbase, lane, g, g_first);
+    for (int g = 1; g < NG; ++g) add_group<S, false, SPREAD>(acc, tab, gen, vbase, lane, g, g_first, lane_off);
   } else {
     float comp[R][S::kVecElems];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
       float part[R][S::kVecElems];
-      add_group<S, true>(part, tab, gen, vbase, lane, g0, g_first);
+      add_group<S, true, false>(part, tab, gen, vbase, lane, g0, g_first, lane_off);
       const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
-      for (uint32_t g = g0 + 1; g < g1; ++g) add_group<S, false>(part, tab, gen, vbase, lane, g, g_first);
+      for (uint32_t g = g0 + 1; g < g1; ++g)
+        add_group<S, false, false>(part, tab, gen, vbase, lane, g, g_first, lane_off);
 #pragma unroll
       for (int u = 0; u < R; ++u)
 #pragma unroll
@@ -584,6 +624,7 @@ __device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S:
 }
 
 // Same sum for one tile on the element-wise path (one lane, all 16 elements).
+template <bool SPREAD>
 __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab, const Gen& gen, uint64_t t,
                                           uint32_t n_groups, uint32_t g_first) {
   float comp[kTile];
@@ -595,7 +636,8 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
       const uint32_t x[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
       for (int j = 0; j < (int)kTile; ++j) {
-        const float v = tab[256u * g + word_byte(x[j >> 2], j & 3)];
+        const uint32_t byte = word_byte(x[j >> 2], j & 3);
+        const float v = SPREAD ? tab[64u * byte + 32u * g + (threadIdx.x & 31u)] : tab[256u * g + byte];
         part[j] = g == g0 ? v : part[j] + v;
       }
     }
@@ -620,14 +662,17 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 // RESTORE: theta + eps_r z_r - lr * sum (the last probe's restore merged with the update):
 // t = fl(theta + delta_r), then t - fl(lr * sum). The restore probe's words are generated
 // after the group loop (reusing the loop's words would keep them live across it).
-template <class S, int NG, bool RESTORE, int N>
+template <class S, int NG, bool RESTORE, int N, bool SPREAD>
 __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
                                                        uint32_t n_groups, Coefs cf, float lr, Probe r) {
-  // n_groups x 256 floats: static for a fixed group count (constant LDS offsets), else dynamic.
+  // n_groups x 256 floats (SPREAD: the interleaved copies): static for a fixed group count
+  // (constant LDS offsets), else dynamic.
   extern __shared__ float tab_dyn[];
-  __shared__ float tab_fix[NG > 0 ? NG * 256 : 1];
+  __shared__ float tab_fix[NG > 0 ? (SPREAD ? kSpreadFloats : NG * 256) : 1];
   float* tab = NG > 0 ? tab_fix : tab_dyn;
-  build_tables(tab, cf, k_base, K, n_groups);
+  // the tables are built while each wave's first loads are in flight (for_each_group's prologue)
+  auto build = [&]() { build_tables<SPREAD>(tab, cf, k_base, K, n_groups); };
+  const uint32_t lane_off = 4u * (threadIdx.x & 31u);  // the lane's copy of a spread table
   const uint32_t g_first = k_base / 8;
   constexpr int R = GroupShape<S>::kRows;
   // two groups in flight for the table counts that stream at one or two workgroups per CU;
@@ -635,7 +680,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
   constexpr int kAhead = NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
   for_each_group<S, kAhead, N>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
-    group_sums<S, NG>(acc, tab, gen, vbase, lane, n_groups, g_first);
+    group_sums<S, NG, SPREAD>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off);
     uint32_t Wr[R][S::kWords];  // the restore probe's generator words
     if (RESTORE) group_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
@@ -649,10 +694,10 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
       }
       d[u] = S::pack(v);
     }
-  });
+  }, build);
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
-    tile_sums(acc, tab, gen, t, n_groups, g_first);
+    tile_sums<SPREAD>(acc, tab, gen, t, n_groups, g_first);
     const uint4 rr = RESTORE ? gen.block(t, r.group) : make_uint4(0, 0, 0, 0);
     const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
     tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
@@ -677,11 +722,13 @@ __global__ __launch_bounds__(kBlock) void gen_bits_kernel(uint8_t* out, uint64_t
 constexpr int kSegsPerLaunch = 64;                 // segments per batched launch (kernel arguments, ~5 KiB)
 constexpr uint64_t kMaxLaunchChunks = 1ull << 31;  // chunks per launch: 32-bit indices with room for the stride
 
-uint32_t cap_blocks() { return g_max_blocks ? g_max_blocks : kDefaultMaxBlocks; }
+// The grid's cap: zo_set_max_blocks if set, else kDefaultMaxBlocks, or (sized) none: the
+// caller then sized work_items per workgroup itself.
+uint32_t cap_blocks(bool sized = false) { return g_max_blocks ? g_max_blocks : sized ? (1u << 30) : kDefaultMaxBlocks; }
 
-uint32_t grid_for(uint64_t work_items, uint64_t per_block) {
+uint32_t grid_for(uint64_t work_items, uint64_t per_block, bool sized = false) {
   const uint64_t need = (work_items + per_block - 1) / per_block;
-  const uint64_t cap = cap_blocks();
+  const uint64_t cap = cap_blocks(sized);
   const uint64_t g = need < cap ? need : cap;
   return static_cast<uint32_t>(g ? g : 1);
 }
@@ -743,10 +790,13 @@ void add_plan(Plans<N>& ps, const Plan& pl) {
   ps.edge_end[s] = (s ? ps.edge_end[s - 1] : 0) + pl.head_nt + pl.tail_nt;
 }
 
+// chunks_per_wave > 0: one workgroup per kWavesPerBlock * chunks_per_wave chunks; 0: up to
+// kDefaultMaxBlocks workgroups, grid-stride beyond.
 template <int N>
-uint32_t plans_grid(const Plans<N>& ps) {
+uint32_t plans_grid(const Plans<N>& ps, uint32_t chunks_per_wave) {
   const uint32_t chunks = ps.chunk_end[ps.count - 1], edges = ps.edge_end[ps.count - 1];
-  const uint32_t a = chunks ? grid_for(chunks, kWavesPerBlock) : 1;
+  const uint32_t a =
+      chunks ? grid_for(chunks, uint64_t{kWavesPerBlock} * (chunks_per_wave ? chunks_per_wave : 1), chunks_per_wave > 0) : 1;
   const uint32_t b = grid_for(edges, kBlock);
   return a > b ? a : b;
 }
@@ -782,17 +832,22 @@ struct Sweep {
 // kernel on OPT-13B shaped bf16 and 3 G-element fp32 buffers. Updates with more probe groups
 // (K >= 32 in bf16, K >= 56 in fp32) are bound by the generator or the LDS table lookups
 // and keep 4 KiB chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity
-// Cache.
+// Cache. Grids: up to kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of
+// many short-lived workgroups keeps the streams compact; a persistent grid of one workgroup
+// per CU measured 5.6 TB/s), except that the one-probe bf16 perturb runs one chunk per wave
+// (OPT-13B: 6.48 -> 6.67 TB/s, OPT-30B: 6.20 -> 6.60; the other kernels measured equal or
+// slower so, the K = 16 update 5.85 against 6.4 TB/s).
 struct Shape {
   uint32_t chunk_groups;
-  uint32_t blocks_per_cu;  // 0: no cap
+  uint32_t blocks_per_cu;    // 0: no cap
+  uint32_t chunks_per_wave;  // 0: up to kDefaultMaxBlocks workgroups, grid-stride beyond
 };
 
 constexpr uint64_t kStreamBytes = 256ull << 20;
 
 Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   const uint64_t group_bytes = kGroupElems * elem;
-  const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0};
+  const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0, 0};
   if (elements * elem < kStreamBytes) return short_chunks;
   uint32_t cap = 1;  // the perturb kernels, one or two probes
   if (w.update) {
@@ -803,7 +858,8 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
       cap = g <= 3 ? 1 : g == 4 ? 2 : g <= 6 ? 3 : 0;
   }
   if (cap == 0) return short_chunks;
-  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap};
+  const bool one_probe_bf16 = !w.update && !w.two && elem == 2;
+  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap, one_probe_bf16 ? 1u : 0u};
 }
 
 // Dynamic LDS that, with `static_lds` bytes of the kernel's own, admits exactly `cap`
@@ -814,17 +870,19 @@ size_t occupancy_lds(uint32_t cap, size_t static_lds) {
   return per_block > static_lds ? per_block - static_lds : 0;
 }
 
-// Dynamic LDS above 64 KiB must be allowed per kernel before the launch.
+// A workgroup's LDS above 64 KiB (static plus dynamic) must be allowed per kernel before the
+// launch.
 template <class K>
-void allow_lds(K kernel, size_t bytes) {
-  if (bytes > 65536)
+void allow_lds(K kernel, size_t dynamic_bytes, size_t static_bytes = 0) {
+  if (dynamic_bytes + static_bytes > 65536)
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              static_cast<int>(bytes));
+                              static_cast<int>(dynamic_bytes));
 }
 
 template <class S, int N>
-void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, uint32_t cap, hipStream_t st) {
-  const dim3 grid(plans_grid(ps)), block(kBlock);
+void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shape& sh, hipStream_t st) {
+  const uint32_t cap = sh.blocks_per_cu;
+  const dim3 grid(plans_grid(ps, sh.chunks_per_wave)), block(kBlock);
   if (!w.update) {
     const size_t pad = occupancy_lds(cap, 0);
     auto go = [&](auto kernel, Probe b) {
@@ -841,31 +899,34 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, uint32_t c
     return;
   }
   const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
-  const size_t table_bytes = static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
-  const size_t pad = occupancy_lds(cap, fixed ? table_bytes : 0);
+  // spread tables where two groups (one in fp32) stream at a capped occupancy, the cases they
+  // measured faster (64 KiB per workgroup would limit an uncapped launch to two workgroups per
+  // CU; a single bf16 group leaves the shared table's LDS half idle and gains nothing)
+  const bool spread = cap > 0 && (w.n_groups == 2 || (w.n_groups == 1 && sizeof(typename S::storage) == 4));
+  const size_t table_bytes =
+      spread ? size_t{kSpreadFloats} * sizeof(float) : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
+  const size_t static_lds = fixed ? table_bytes : 0;
+  const size_t pad = occupancy_lds(cap, static_lds);
   const size_t tables = fixed ? 0 : table_bytes;
   const size_t lds = tables > pad ? tables : pad;  // dynamic tables (up to 128 KiB) or the pad
   auto go = [&](auto kernel) {
-    allow_lds(kernel, lds);
+    allow_lds(kernel, lds, static_lds);
     kernel<<<grid, block, lds, st>>>(ps, gen, w.k_base, w.K, w.n_groups, w.cf, w.lr, w.r);
   };
-  if (w.restore) {
+  auto dispatch = [&](auto restore) {
+    constexpr bool R = decltype(restore)::value;
     switch (w.n_groups) {
-      case 1: go(update_kernel<S, 1, true, N>); break;
-      case 2: go(update_kernel<S, 2, true, N>); break;
-      case 4: go(update_kernel<S, 4, true, N>); break;
-      case 8: go(update_kernel<S, 8, true, N>); break;
-      default: go(update_kernel<S, 0, true, N>); break;
+      case 1: spread ? go(update_kernel<S, 1, R, N, true>) : go(update_kernel<S, 1, R, N, false>); break;
+      case 2: spread ? go(update_kernel<S, 2, R, N, true>) : go(update_kernel<S, 2, R, N, false>); break;
+      case 4: go(update_kernel<S, 4, R, N, false>); break;
+      case 8: go(update_kernel<S, 8, R, N, false>); break;
+      default: go(update_kernel<S, 0, R, N, false>); break;
     }
-  } else {
-    switch (w.n_groups) {
-      case 1: go(update_kernel<S, 1, false, N>); break;
-      case 2: go(update_kernel<S, 2, false, N>); break;
-      case 4: go(update_kernel<S, 4, false, N>); break;
-      case 8: go(update_kernel<S, 8, false, N>); break;
-      default: go(update_kernel<S, 0, false, N>); break;
-    }
-  }
+  };
+  if (w.restore)
+    dispatch(std::true_type{});
+  else
+    dispatch(std::false_type{});
 }
 
 int check_sweep(const Sweep& w) {
@@ -908,7 +969,7 @@ int run_one(void* params, uint64_t offset, uint64_t n, uint64_t seed, uint32_t s
   ps.chunk_groups = sh.chunk_groups;
   add_plan(ps, make_plan(params, offset, n, sizeof(typename S::storage), sh.chunk_groups));
   (void)hipGetLastError();
-  launch_sweep<S>(ps, make_gen(seed, step), w, sh.blocks_per_cu, static_cast<hipStream_t>(stream));
+  launch_sweep<S>(ps, make_gen(seed, step), w, sh, static_cast<hipStream_t>(stream));
   return launch_status();
 }
 
@@ -961,19 +1022,19 @@ int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_
     if (segs[i].n == 0) continue;
     const Plan pl = make_plan(segs[i].params, segs[i].offset, segs[i].n, sizeof(typename S::storage), sh.chunk_groups);
     if (ps.count && ps.chunk_end[ps.count - 1] + static_cast<uint64_t>(plan_chunks(pl, sh.chunk_groups)) >= kMaxLaunchChunks) {
-      launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);  // keep a launch's chunk count 32-bit
+      launch_sweep<S>(ps, gen, w, sh, st);  // keep a launch's chunk count 32-bit
       if (launch_status() != ZO_OK) return ZO_ERR_HIP;
       ps.count = 0;
     }
     add_plan(ps, pl);
     if (ps.count == kSegsPerLaunch) {
-      launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);
+      launch_sweep<S>(ps, gen, w, sh, st);
       if (launch_status() != ZO_OK) return ZO_ERR_HIP;
       ps.count = 0;
     }
   }
   if (ps.count) {
-    launch_sweep<S>(ps, gen, w, sh.blocks_per_cu, st);
+    launch_sweep<S>(ps, gen, w, sh, st);
     return launch_status();
   }
   return ZO_OK;
