@@ -702,6 +702,62 @@ def test_full_size_sampled_windows(name, K):
                                         tr[lo:hi], c, w.lr, w.eps, "bf16")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("K", [8, 16, 24, 32, 48, 64])
+def test_streaming_shapes_sampled_windows(dtype, K):
+    """Every launch shape the library picks above the 256 MiB streaming threshold (perturb with
+    one probe, two probes in one group and in two groups, update and update-with-restore with
+    1 to 8 probe groups: spread or shared tables, 1-4 workgroups per CU or full occupancy, one
+    or two groups in flight), for bf16 and fp32, on a ragged 288 MB buffer at global offset
+    777: ten windows of 2^15 weights (the first, the last with the ragged tail, eight at random
+    offsets) checked against the oracle after every sweep."""
+    n = (144_000_019 if dtype == "bf16" else 72_000_011)
+    off, seed, step, eps, lr = 777, 41, 6, 1e-3, 1e-3
+    note(f"streaming shapes: {dtype} n {n} K {K}")
+    t = torch.empty(n, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device=DEV)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(43)
+    t.normal_(0.0, 0.02, generator=gen)
+    size = 1 << 15
+    rng = np.random.default_rng(K)
+    wins = sorted({0, n - size} | {int(x) for x in rng.integers(0, n - size, 8)})
+    if dtype == "bf16":
+        grab = lambda: [host_bits(t[s:s + size]) for s in wins]
+    else:
+        grab = lambda: [t[s:s + size].cpu().numpy() for s in wins]
+    c = rng.standard_normal(K).astype(np.float32)
+    kr = K - 1  # restore probe inside the update's last group
+    states = [grab()]
+    zo.zo_perturb(t, 3, eps, seed, step, offset=off)
+    states.append(grab())
+    zo.zo_perturb2(t, 3, -2 * eps, 4, eps, seed, step, offset=off)  # one probe group
+    states.append(grab())
+    zo.zo_perturb2(t, 4, eps, 12, eps, seed, step, offset=off)  # two probe groups
+    states.append(grab())
+    zo.zo_update_ex(t, c, lr, seed, step, offset=off)
+    states.append(grab())
+    zo.zo_update_restore(t, c, lr, seed, step, kr, eps, offset=off)
+    states.append(grab())
+    torch.cuda.synchronize()
+    del t
+    torch.cuda.empty_cache()
+    for i, s in enumerate(wins):
+        b, p1, p2, p3, u, ur = (st[i] for st in states)
+        g = off + s
+        np.testing.assert_array_equal(p1, oracle.perturb(b, dtype, g, seed, step, 3, eps), err_msg=f"window {s}")
+        np.testing.assert_array_equal(p2, oracle.perturb2(p1, dtype, g, seed, step, 3, -2 * eps, 4, eps),
+                                      err_msg=f"window {s}")
+        np.testing.assert_array_equal(p3, oracle.perturb2(p2, dtype, g, seed, step, 4, eps, 12, eps),
+                                      err_msg=f"window {s}")
+        want_u = oracle.update(p3, dtype, g, seed, step, c, lr)
+        want_ur = oracle.update_restore(u, dtype, g, seed, step, c, lr, kr, eps)
+        if dtype == "bf16":
+            assert_bf16_within_1ulp(u, want_u, p3, c, lr)
+        else:
+            assert_f32_update_close(u, want_u, c, lr)
+        assert_restore_update_close(ur, want_ur, u, c, lr, eps, dtype)
+
+
 def test_full_size_separate_tensors():
     """OPT-13B as 644 separately allocated tensors, in the benchmark's per-tensor launch
     configuration (batches of 64 tensors per launch): a segmented perturb, two-probe transition,
