@@ -17,19 +17,23 @@
 // instructions) and fp32 lane groups transpose a 4x4 word matrix (four instructions). A wave
 // streams a chunk of consecutive row groups (up to 32 KiB) with the loads of the next one or
 // two groups in flight while it works on the current one, and large sweeps cap the
-// workgroups per CU (few long read-write streams keep HBM busiest). Head and tail elements
-// that do not fill a row group (and everything, when the storage is not 16-byte aligned
-// relative to the global index) take an element-wise path, one tile per lane.
+// workgroups per CU (few long read-write streams keep HBM busiest). The loops are written so
+// that the compiler's memory waits are exact, and the lightest perturbs are paced explicitly.
+// Head and tail elements that do not fill a row group (and everything, when the storage is
+// not 16-byte aligned relative to the global index) take an element-wise path, one tile per
+// lane.
 //
 // zo_perturb_segments / zo_update_segments sweep a list of separate tensors: the host validates
 // the list, builds one plan per tensor and launches batches of up to 64 plans (kernel
 // arguments); inside a launch the chunks and edge tiles of all its tensors are numbered
-// consecutively and each wave maps its chunk to a tensor with a forward-only cursor.
+// consecutively and each wave finds its chunk's tensor by a binary search.
 //
 // The update keeps, per probe group, a 256-entry table in LDS: entry b is the signed sum of
 // the group's 8 coefficients selected by the bits of b (pairwise). Applying 8 probes to an
-// element costs a byte extract and an LDS read. Groups accumulate in fp32, sequentially
-// within runs of 8 groups and with Neumaier compensation across runs.
+// element costs a byte extract and an LDS read; with one or two groups in a streaming launch
+// the tables are spread over 32 copies so that each lane reads its own LDS bank. Groups
+// accumulate in fp32, sequentially within runs of 8 groups and with Neumaier compensation
+// across runs.
 //
 // Built with -ffp-contract=off: every product and sum is rounded as written.
 
@@ -49,9 +53,9 @@ namespace {
 constexpr uint32_t kTile = 16;    // elements per generator block
 constexpr uint32_t kBlock = 256;  // threads per workgroup (4 waves)
 constexpr uint32_t kWavesPerBlock = kBlock / 64;
-// s_waitcnt immediate for vmcnt(2) that leaves expcnt and lgkmcnt unconstrained (gfx9
-// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
-constexpr int kWaitVmcnt2 = 0x0F72;
+// s_waitcnt immediate for vmcnt(n), n < 16, that leaves expcnt and lgkmcnt unconstrained
+// (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+constexpr int wait_vmcnt(int n) { return 0x0F70 | n; }
 constexpr uint64_t kGroupElems = 1024;      // elements per row group (one Philox block per lane)
 constexpr uint64_t kMaxChunkBytes = 32768;  // bytes a wave streams per chunk, at most
 constexpr uint32_t kDefaultMaxBlocks = 65536;
@@ -319,16 +323,18 @@ __device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupSh
 // wave per chunk walks the chunk's groups in address order with the loads of the next AHEAD
 // groups in flight while the body works on the current one (each wave streams up to 32 KiB,
 // reads and writes interleaved). A wave's chunk indices increase, so its segment cursor
-// only moves forward. PACED (two ahead only): each step of three groups first waits until
-// its newest prefetch is all the wave has outstanding, earlier stores included. The
-// lightest sweeps stream HBM faster paced (the one-probe bf16 perturb: 6.57 TB/s against
-// 6.40 with every request the loop allows in flight), heavier ones need the overlap.
+// only moves forward. PACE > 0 (two ahead only): each step of three groups first waits until
+// at most PACE memory operations of the wave are outstanding: with 2, only the step's own
+// prefetch; with 4, also the previous step's last stores. The lightest sweeps stream HBM
+// faster paced (OPT-13B bf16 perturb: 6.40 TB/s with every request the loop allows in
+// flight, 6.67 paced at 2, 6.76 at 4; pacing at 6 or 8 measured lower), heavier ones need
+// the overlap.
 // prologue() runs once per wave, after the loads of the wave's first group are issued (at
 // once for a wave without chunks), so that work such as building the update's LDS tables
 // overlaps their latency; it may hold a workgroup barrier, which every wave reaches once.
-template <class S, int AHEAD, int N, bool PACED = false, class Body, class Prologue>
+template <class S, int AHEAD, int N, int PACE = 0, class Body, class Prologue>
 __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Prologue prologue) {
-  static_assert(!PACED || AHEAD == 2, "pacing applies to the two-ahead loop");
+  static_assert(PACE == 0 || (AHEAD == 2 && PACE >= 2 && PACE < 16), "pacing applies to the two-ahead loop");
   static_assert(AHEAD == 1 || AHEAD == 2, "one or two groups in flight");
   using G = GroupShape<S>;
   const uint32_t n_waves = gridDim.x * kWavesPerBlock;
@@ -394,7 +400,7 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Pr
     } else {
       auto step3 = [&]() {
         prefetch(z, 2);
-        if constexpr (PACED) __builtin_amdgcn_s_waitcnt(kWaitVmcnt2);  // only z's loads stay in flight
+        if constexpr (PACE > 0) __builtin_amdgcn_s_waitcnt(wait_vmcnt(PACE));
         work(x, g);
         prefetch(x, 2);
         work(y, g + 1);
@@ -458,14 +464,14 @@ struct Probe {
   __device__ __forceinline__ float delta(uint32_t byte) const { return ((byte >> bit) & 1u) ? eps : -eps; }
 };
 
-template <class S, bool TWO, int N, bool PACED>
+template <class S, bool TWO, int N, int PACE>
 __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, Probe a, Probe b) {
   extern __shared__ uint32_t occupancy_pad[];  // dynamic LDS only limits workgroups per CU
   if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count <= 64)
   constexpr int R = GroupShape<S>::kRows;
   const bool shared_group = a.group == b.group;
   auto no_prologue = []() {};
-  for_each_group<S, 2, N, PACED>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+  for_each_group<S, 2, N, PACE>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     uint32_t Wa[R][S::kWords], Wb[R][S::kWords];
     group_words(gen, vbase, lane, a.group, Wa, S());
     if (TWO) {
@@ -889,13 +895,16 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
       allow_lds(kernel, pad);
       kernel<<<grid, block, pad, st>>>(ps, gen, w.a, b);
     };
-    // paced when the generator work per byte is lightest: one probe group, or fp32 with two
+    // paced when the generator work per byte is lightest: one probe group, or fp32 with two;
+    // bf16 at 4 outstanding operations (one probe +1.3%, two in one group +3.4% over 2), fp32
+    // at 2 (4 measured equal or lower)
+    constexpr int kPace = sizeof(typename S::storage) == 2 ? 4 : 2;
     const bool two_groups = w.two && w.a.group != w.b.group;
     const bool paced = (two_groups ? 2u : 1u) * (sizeof(typename S::storage) == 2 ? 2u : 1u) <= 2u;
     if (w.two)
-      paced ? go(perturb_kernel<S, true, N, true>, w.b) : go(perturb_kernel<S, true, N, false>, w.b);
+      paced ? go(perturb_kernel<S, true, N, kPace>, w.b) : go(perturb_kernel<S, true, N, 0>, w.b);
     else
-      paced ? go(perturb_kernel<S, false, N, true>, w.a) : go(perturb_kernel<S, false, N, false>, w.a);
+      paced ? go(perturb_kernel<S, false, N, kPace>, w.a) : go(perturb_kernel<S, false, N, 0>, w.a);
     return;
   }
   const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
