@@ -108,10 +108,10 @@ int zo_probe_coeffs_ex(const double* L_plus, const double* L_minus, uint32_t K, 
  * The fused form of section 4.2 (Eq. 6, Delta theta = -eta Z W Delta l) and of
  * Algorithm 1's per-probe loop: one read and one write of theta for all K probes, which
  * are regenerated in registers. c: host array of K floats (from zo_probe_coeffs).
- * Arithmetic: per element, sum_k c[k] z_k in fp32 (pairwise within each group of 8 probes,
- * sequential across groups within runs of 8 groups, compensated across runs),
- * s = fl(lr * sum), theta - s in fp32, then one
- * rounding to bf16 for bf16 weights. With K = 1 this equals zo_perturb(k = 0,
+ * Arithmetic: per element, s = sum over the probe groups of fl(lr * t_g) in fp32, where t_g is
+ * the pairwise fp32 sum of the element's 8 signed c[k] of group g (sequential across groups
+ * within runs of 8 groups, compensated across runs); theta - s in fp32, then one rounding
+ * to bf16 for bf16 weights. With K = 1 this equals zo_perturb(k = 0,
  * eps = -fl(lr * c[0])) bit for bit.
  * Errors: ZO_ERR_NULL (params NULL with n > 0, c NULL with K > 0), ZO_ERR_ARG (dtype,
  * alignment, K > ZO_K_MAX, k_base + K > 2^32), ZO_ERR_NONFINITE (lr or any c[k]), ZO_ERR_HIP.
@@ -149,7 +149,7 @@ int zo_perturb2(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint6
  *                                  - lr * sum_j c[j] z_{k_base+j}[offset+i], one sweep:
  * the last probe's restore merged with the fused update (Algorithm 1's final +eps and its
  * rank-0 update loop; section 4.2, Eq. 6). Arithmetic per element in fp32:
- * t = fl(theta + eps_restore z), then t - fl(lr * sum) as in zo_update, then one rounding to
+ * t = fl(theta + eps_restore z), then t - s with s as in zo_update, then one rounding to
  * bf16 for bf16 weights. eps_restore = 0 gives zo_update_ex's result bit for bit.
  * Errors: as zo_update_ex (ZO_ERR_NONFINITE also for a non-finite eps_restore). With K = 0
  * it applies the restore alone.

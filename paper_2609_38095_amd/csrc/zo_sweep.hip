@@ -28,9 +28,9 @@
 // arguments); inside a launch the chunks and edge tiles of all its tensors are numbered
 // consecutively and each wave finds its chunk's tensor by a binary search.
 //
-// The update keeps, per probe group, a 256-entry table in LDS: entry b is the signed sum of
-// the group's 8 coefficients selected by the bits of b (pairwise). Applying 8 probes to an
-// element costs a byte extract and an LDS read; with one or two groups in a streaming launch
+// The update keeps, per probe group, a 256-entry table in LDS: entry b is lr times the signed
+// sum of the group's 8 coefficients selected by the bits of b (pairwise), so applying 8 probes
+// to an element costs a byte extract and an LDS read, and the step is one subtraction; with one or two groups in a streaming launch
 // the tables are spread over 32 copies so that each lane reads its own LDS bank. Groups
 // accumulate in fp32, sequentially within runs of 8 groups and with Neumaier compensation
 // across runs.
@@ -525,14 +525,16 @@ struct Coefs {
 constexpr uint32_t kSpreadFloats = 256 * 64;
 
 // Build the n_groups x 256 table in LDS (SPREAD: the 32 interleaved copies). Entry (g, b):
-// sum over the group's 8 probe slots of +-c (bit set: +c); slots outside [k_base, k_base + K)
-// contribute 0; pairwise. Thread b writes entry b of every group: the group loop and the
+// fl(lr * t), t the sum over the group's 8 probe slots of +-c (bit set: +c), pairwise; slots
+// outside [k_base, k_base + K) contribute 0. Scaling each entry once here saves the sweep a
+// multiply per element; with one probe the entry is +-fl(lr * c), the step a perturb by
+// -fl(lr * c) would apply. Thread b writes entry b of every group: the group loop and the
 // coefficient reads are uniform (scalar loads), and the sign of slot s is an XOR of the
 // coefficient's sign bit with bit s of ~b.
 static_assert(kBlock == 256, "one table entry per thread");
 template <bool SPREAD>
 __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
-                                             uint32_t n_groups) {
+                                             uint32_t n_groups, float lr) {
   const uint32_t b = threadIdx.x;
   uint32_t flip[8];
 #pragma unroll
@@ -546,7 +548,7 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
       const float cv = (k >= k_base && k - k_base < K) ? cf.c[k - k_base] : 0.0f;
       v[s] = __uint_as_float(__float_as_uint(cv) ^ flip[s]);
     }
-    const float t = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+    const float t = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]))) * lr;
     if constexpr (SPREAD) {
       const float4 t4 = make_float4(t, t, t, t);
 #pragma unroll
@@ -566,13 +568,14 @@ __device__ __forceinline__ float spread_at(const float* tab, uint32_t lane_off, 
   return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + addr + 128u * g);
 }
 
-// acc[u][e] (+)= table value of probe group g for each element of the row group.
+// acc[u][e] (+)= table value of probe group g for each element of the row group; W receives
+// the group's generator words.
 template <class S, bool FIRST, bool SPREAD>
 __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                           const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t g,
-                                          uint32_t g_first, uint32_t lane_off) {
+                                          uint32_t g_first, uint32_t lane_off,
+                                          uint32_t (&W)[GroupShape<S>::kRows][S::kWords]) {
   constexpr int R = GroupShape<S>::kRows;
-  uint32_t W[R][S::kWords];
   group_words(gen, vbase, lane, g_first + g, W, S());
   const float* tg = tab + 256u * g;
 #pragma unroll
@@ -589,25 +592,29 @@ __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::
 }
 
 // Sum of the tables of probe groups 0 .. n_groups-1 for the row group: NG > 0 fixes the count
-// at compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
+// at compile time (one run) and leaves the last group's generator words in Wlast; NG == 0:
+// runs of 8 groups, Neumaier-compensated across runs (Wlast is not written).
 template <class S, int NG, bool SPREAD>
 __device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                            const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t n_groups,
-                                           uint32_t g_first, uint32_t lane_off) {
+                                           uint32_t g_first, uint32_t lane_off,
+                                           uint32_t (&Wlast)[GroupShape<S>::kRows][S::kWords]) {
   constexpr int R = GroupShape<S>::kRows;
   static_assert(!SPREAD || NG == 1 || NG == 2, "spread tables hold one or two groups");
   if constexpr (NG > 0) {
-    add_group<S, true, SPREAD>(acc, tab, gen, vbase, lane, 0, g_first, lane_off);
+    add_group<S, true, SPREAD>(acc, tab, gen, vbase, lane, 0, g_first, lane_off, Wlast);
 #pragma unroll
-    for (int g = 1; g < NG; ++g) add_group<S, false, SPREAD>(acc, tab, gen, vbase, lane, g, g_first, lane_off);
+    for (int g = 1; g < NG; ++g)
+      add_group<S, false, SPREAD>(acc, tab, gen, vbase, lane, g, g_first, lane_off, Wlast);
   } else {
     float comp[R][S::kVecElems];
+    uint32_t W[R][S::kWords];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
       float part[R][S::kVecElems];
-      add_group<S, true, false>(part, tab, gen, vbase, lane, g0, g_first, lane_off);
+      add_group<S, true, false>(part, tab, gen, vbase, lane, g0, g_first, lane_off, W);
       const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
       for (uint32_t g = g0 + 1; g < g1; ++g)
-        add_group<S, false, false>(part, tab, gen, vbase, lane, g, g_first, lane_off);
+        add_group<S, false, false>(part, tab, gen, vbase, lane, g, g_first, lane_off, W);
 #pragma unroll
       for (int u = 0; u < R; ++u)
 #pragma unroll
@@ -666,8 +673,11 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 }
 
 // RESTORE: theta + eps_r z_r - lr * sum (the last probe's restore merged with the update):
-// t = fl(theta + delta_r), then t - fl(lr * sum). The restore probe's words are generated
-// after the group loop (reusing the loop's words would keep them live across it).
+// t = fl(theta + delta_r), then t minus the sum of the lr-scaled table values. When the count of
+// groups is fixed and the restore probe lies in the last of them (Algorithm 1 restores the
+// step's last probe), its generator words are those the group sum has just produced; otherwise
+// they are generated after the group loop (keeping a middle group's words would hold them live
+// across the rest of it).
 template <class S, int NG, bool RESTORE, int N, bool SPREAD>
 __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
                                                        uint32_t n_groups, Coefs cf, float lr, Probe r) {
@@ -677,18 +687,19 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
   __shared__ float tab_fix[NG > 0 ? (SPREAD ? kSpreadFloats : NG * 256) : 1];
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   // the tables are built while each wave's first loads are in flight (for_each_group's prologue)
-  auto build = [&]() { build_tables<SPREAD>(tab, cf, k_base, K, n_groups); };
+  auto build = [&]() { build_tables<SPREAD>(tab, cf, k_base, K, n_groups, lr); };
   const uint32_t lane_off = 4u * (threadIdx.x & 31u);  // the lane's copy of a spread table
   const uint32_t g_first = k_base / 8;
   constexpr int R = GroupShape<S>::kRows;
   // two groups in flight for the table counts that stream at one or two workgroups per CU;
   // one for the heavier updates, which run more waves per CU
   constexpr int kAhead = NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
+  const bool restore_in_last = NG > 0 && r.group == g_first + static_cast<uint32_t>(NG) - 1;  // uniform
   for_each_group<S, kAhead, N>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
-    group_sums<S, NG, SPREAD>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off);
-    uint32_t Wr[R][S::kWords];  // the restore probe's generator words
-    if (RESTORE) group_words(gen, vbase, lane, r.group, Wr, S());
+    uint32_t Wr[R][S::kWords];  // the last group's words, then the restore probe's
+    group_sums<S, NG, SPREAD>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off, Wr);
+    if (RESTORE && !restore_in_last) group_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
     for (int u = 0; u < R; ++u) {
       float v[S::kVecElems];
@@ -696,7 +707,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
 #pragma unroll
       for (int e = 0; e < S::kVecElems; ++e) {
         if (RESTORE) v[e] = v[e] + r.delta(elem_byte<S>(Wr[u], e));
-        v[e] = v[e] - lr * acc[u][e];
+        v[e] = v[e] - acc[u][e];
       }
       d[u] = S::pack(v);
     }
@@ -708,7 +719,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
     const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
     tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
       if (RESTORE) v = v + r.delta(word_byte(xr[e >> 2], e & 3));
-      return v - lr * acc[e];
+      return v - acc[e];
     });
   });
 }
@@ -840,9 +851,10 @@ struct Sweep {
 // and keep 4 KiB chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity
 // Cache. Grids: up to kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of
 // many short-lived workgroups keeps the streams compact; a persistent grid of one workgroup
-// per CU measured 5.6 TB/s), except that the one-probe bf16 perturb runs one chunk per wave
-// (OPT-13B: 6.48 -> 6.67 TB/s, OPT-30B: 6.20 -> 6.60; the other kernels measured equal or
-// slower so, the K = 16 update 5.85 against 6.4 TB/s).
+// per CU measured 5.6 TB/s), except that the one-probe bf16 perturb and the two-group bf16
+// update with restore run one chunk per wave (OPT-13B: the perturb 6.48 -> 6.67 TB/s, OPT-30B
+// 6.20 -> 6.60; the update with restore 5.94 -> 6.13; the other kernels measured equal or
+// slower so, the K = 16 update 5.93 against 6.45 TB/s).
 struct Shape {
   uint32_t chunk_groups;
   uint32_t blocks_per_cu;    // 0: no cap
@@ -865,7 +877,9 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   }
   if (cap == 0) return short_chunks;
   const bool one_probe_bf16 = !w.update && !w.two && elem == 2;
-  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap, one_probe_bf16 ? 1u : 0u};
+  const bool restore_two_groups_bf16 = w.update && w.restore && w.n_groups == 2 && elem == 2;
+  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap,
+               one_probe_bf16 || restore_two_groups_bf16 ? 1u : 0u};
 }
 
 // Dynamic LDS that, with `static_lds` bytes of the kernel's own, admits exactly `cap`
