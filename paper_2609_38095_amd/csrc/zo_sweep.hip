@@ -550,9 +550,13 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
     }
     const float t = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]))) * lr;
     if constexpr (SPREAD) {
+      // entry b's 8 float4 of copies, 256 bytes after entry b - 1's: thread b writes them
+      // starting at float4 b mod 8, so that the 64 lanes of each write cover every bank 8 times
+      // (in a fixed order all 64 would land on the same 4 banks)
       const float4 t4 = make_float4(t, t, t, t);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) *reinterpret_cast<float4*>(tab + 64u * b + 32u * g + 4u * q) = t4;
+      for (int q = 0; q < 8; ++q)
+        *reinterpret_cast<float4*>(tab + 64u * b + 32u * g + 4u * ((q + b) & 7u)) = t4;
     } else {
       tab[256u * g + b] = t;
     }

@@ -363,6 +363,9 @@ RESTORE_CASES = [
     # n, offset, k_base, K, k_restore
     (50_000, 0, 0, 16, 15), (20_000, 5, 0, 4, 3), (30_000, 0, 0, 64, 63), (9_000, 2 ** 33, 0, 200, 199),
     (10_000, 0, 0, 16, 40), (10_000, 0, 8, 16, 0), (7_000, 0, 3, 13, 15), (5_000, 0, 0, 0, 2),
+    # restore probe inside the update's groups but not in the last one (its words are generated
+    # again rather than taken from the group sum)
+    (12_000, 0, 0, 16, 3), (12_000, 17, 0, 32, 9), (6_000, 0, 0, 64, 50),
 ]
 
 
