@@ -515,16 +515,23 @@ struct Coefs {
   float c[ZO_K_MAX];
 };
 
-// Spread tables, for one or two probe groups in streaming launches: 32 copies of each
-// 256-entry table, interleaved so that copy r of entry e of group g is float 64 e + 32 g + r.
-// Lane l reads copy l mod 32, which sits in LDS bank l mod 32, so a 64-lane read of random
-// bytes takes 2 LDS cycles instead of about 6.3 when all lanes share one copy. A lookup's
-// byte address, 256 e + 4 (l mod 32) + 128 g, is one byte permute of the generator word and
-// the lane's copy offset (as many instructions as a lookup into a shared table). 64 KiB per
-// workgroup.
+// Spread tables, for streaming launches: C = 32 or 16 copies of each 256-entry table of up to
+// 64 / C groups (64 KiB), interleaved so that copy r of entry e of group g is float
+// 64 e + C g + r. Lane l reads copy l mod C, which sits in LDS bank (C g + l mod C) mod 32:
+// with 32 copies every lane of a half-wave has its own bank, so a 64-lane read of random
+// bytes takes 2 LDS cycles instead of about 6.3 when all lanes share one copy; with 16 copies
+// two lanes share a bank, about 4 cycles. A lookup's byte address, 256 e + 4 (l mod C) + 4 C g,
+// is one byte permute of the generator word and the lane's copy offset (as many instructions
+// as a lookup into a shared table).
 constexpr uint32_t kSpreadFloats = 256 * 64;
+// floats of the tables of NG groups: C interleaved copies, or one shared copy (C = 0)
+template <int NG, int C>
+constexpr uint32_t table_floats() {
+  static_assert(C == 0 || (C == 16 || C == 32) && NG * C <= 64, "spread tables fill at most 64 KiB");
+  return C == 0 ? NG * 256 : kSpreadFloats;
+}
 
-// Build the n_groups x 256 table in LDS (SPREAD: the 32 interleaved copies). Entry (g, b):
+// Build the n_groups x 256 table in LDS (C > 0: the interleaved copies). Entry (g, b):
 // fl(lr * t), t the sum over the group's 8 probe slots of +-c (bit set: +c), pairwise; slots
 // outside [k_base, k_base + K) contribute 0. Scaling each entry once here saves the sweep a
 // multiply per element; with one probe the entry is +-fl(lr * c), the step a perturb by
@@ -532,7 +539,7 @@ constexpr uint32_t kSpreadFloats = 256 * 64;
 // coefficient reads are uniform (scalar loads), and the sign of slot s is an XOR of the
 // coefficient's sign bit with bit s of ~b.
 static_assert(kBlock == 256, "one table entry per thread");
-template <bool SPREAD>
+template <int C>
 __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
                                              uint32_t n_groups, float lr) {
   const uint32_t b = threadIdx.x;
@@ -549,14 +556,15 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
       v[s] = __uint_as_float(__float_as_uint(cv) ^ flip[s]);
     }
     const float t = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]))) * lr;
-    if constexpr (SPREAD) {
-      // entry b's 8 float4 of copies, 256 bytes after entry b - 1's: thread b writes them
-      // starting at float4 b mod 8, so that the 64 lanes of each write cover every bank 8 times
-      // (in a fixed order all 64 would land on the same 4 banks)
+    if constexpr (C > 0) {
+      // entry b's C / 4 float4 of copies, 256 bytes after entry b - 1's: thread b writes them
+      // starting at float4 b mod (C / 4), so that the lanes of each write spread over the banks
+      // the group's copies occupy (in a fixed order all 64 would land on the same 4 banks)
+      constexpr uint32_t Q = C / 4;
+      float* e = tab + 64u * b + C * g;
       const float4 t4 = make_float4(t, t, t, t);
 #pragma unroll
-      for (int q = 0; q < 8; ++q)
-        *reinterpret_cast<float4*>(tab + 64u * b + 32u * g + 4u * ((q + b) & 7u)) = t4;
+      for (uint32_t q = 0; q < Q; ++q) *reinterpret_cast<float4*>(e + 4u * ((q + b) & (Q - 1))) = t4;
     } else {
       tab[256u * g + b] = t;
     }
@@ -564,17 +572,18 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
   __syncthreads();
 }
 
-// Spread-table lookup: one byte permute forms the address (byte 0: the lane's copy offset
-// `lane_off`, byte 1: byte e of w, upper bytes 0), then the float there plus the group's
-// 128-byte offset.
+// Spread-table lookup in group g (C copies): one byte permute forms the address (byte 0: the
+// lane's copy offset `lane_off` = 4 (l mod C), byte 1: byte e of w, upper bytes 0), then the
+// float there plus the group's offset 4 C g.
+template <int C>
 __device__ __forceinline__ float spread_at(const float* tab, uint32_t lane_off, uint32_t w, int e, uint32_t g) {
   const uint32_t addr = __builtin_amdgcn_perm(w, lane_off, 0x0C0C0000u | ((4u + static_cast<uint32_t>(e)) << 8));
-  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + addr + 128u * g);
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + addr + 4u * C * g);
 }
 
 // acc[u][e] (+)= table value of probe group g for each element of the row group; W receives
 // the group's generator words.
-template <class S, bool FIRST, bool SPREAD>
+template <class S, bool FIRST, int C>
 __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                           const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t g,
                                           uint32_t g_first, uint32_t lane_off,
@@ -587,8 +596,8 @@ __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::
 #pragma unroll
     for (int e = 0; e < S::kVecElems; ++e) {
       float x;
-      if constexpr (SPREAD)
-        x = spread_at(tab, lane_off, W[u][e >> 2], e & 3, g);
+      if constexpr (C > 0)
+        x = spread_at<C>(tab, lane_off, W[u][e >> 2], e & 3, g);
       else
         x = table_at(tg, W[u][e >> 2], e & 3);
       acc[u][e] = FIRST ? x : acc[u][e] + x;
@@ -598,27 +607,27 @@ __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::
 // Sum of the tables of probe groups 0 .. n_groups-1 for the row group: NG > 0 fixes the count
 // at compile time (one run) and leaves the last group's generator words in Wlast; NG == 0:
 // runs of 8 groups, Neumaier-compensated across runs (Wlast is not written).
-template <class S, int NG, bool SPREAD>
+template <class S, int NG, int C>
 __device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                            const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t n_groups,
                                            uint32_t g_first, uint32_t lane_off,
                                            uint32_t (&Wlast)[GroupShape<S>::kRows][S::kWords]) {
   constexpr int R = GroupShape<S>::kRows;
-  static_assert(!SPREAD || NG == 1 || NG == 2, "spread tables hold one or two groups");
+  static_assert(C == 0 || NG > 0, "spread tables need a fixed group count");
   if constexpr (NG > 0) {
-    add_group<S, true, SPREAD>(acc, tab, gen, vbase, lane, 0, g_first, lane_off, Wlast);
+    add_group<S, true, C>(acc, tab, gen, vbase, lane, 0, g_first, lane_off, Wlast);
 #pragma unroll
     for (int g = 1; g < NG; ++g)
-      add_group<S, false, SPREAD>(acc, tab, gen, vbase, lane, g, g_first, lane_off, Wlast);
+      add_group<S, false, C>(acc, tab, gen, vbase, lane, g, g_first, lane_off, Wlast);
   } else {
     float comp[R][S::kVecElems];
     uint32_t W[R][S::kWords];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
       float part[R][S::kVecElems];
-      add_group<S, true, false>(part, tab, gen, vbase, lane, g0, g_first, lane_off, W);
+      add_group<S, true, 0>(part, tab, gen, vbase, lane, g0, g_first, lane_off, W);
       const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
       for (uint32_t g = g0 + 1; g < g1; ++g)
-        add_group<S, false, false>(part, tab, gen, vbase, lane, g, g_first, lane_off, W);
+        add_group<S, false, 0>(part, tab, gen, vbase, lane, g, g_first, lane_off, W);
 #pragma unroll
       for (int u = 0; u < R; ++u)
 #pragma unroll
@@ -641,7 +650,7 @@ __device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S:
 }
 
 // Same sum for one tile on the element-wise path (one lane, all 16 elements).
-template <bool SPREAD>
+template <int C>
 __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab, const Gen& gen, uint64_t t,
                                           uint32_t n_groups, uint32_t g_first) {
   float comp[kTile];
@@ -654,7 +663,12 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 #pragma unroll
       for (int j = 0; j < (int)kTile; ++j) {
         const uint32_t byte = word_byte(x[j >> 2], j & 3);
-        const float v = SPREAD ? tab[64u * byte + 32u * g + (threadIdx.x & 31u)] : tab[256u * g + byte];
+        float v;
+        if constexpr (C > 0) {
+          v = tab[64u * byte + C * g + (threadIdx.x % C)];
+        } else {
+          v = tab[256u * g + byte];
+        }
         part[j] = g == g0 ? v : part[j] + v;
       }
     }
@@ -682,27 +696,27 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 // step's last probe), its generator words are those the group sum has just produced; otherwise
 // they are generated after the group loop (keeping a middle group's words would hold them live
 // across the rest of it).
-template <class S, int NG, bool RESTORE, int N, bool SPREAD>
+template <class S, int NG, bool RESTORE, int N, int C>
 __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
                                                        uint32_t n_groups, Coefs cf, float lr, Probe r) {
-  // n_groups x 256 floats (SPREAD: the interleaved copies): static for a fixed group count
+  // n_groups x 256 floats (C > 0: the interleaved copies): static for a fixed group count
   // (constant LDS offsets), else dynamic.
   extern __shared__ float tab_dyn[];
-  __shared__ float tab_fix[NG > 0 ? (SPREAD ? kSpreadFloats : NG * 256) : 1];
+  __shared__ float tab_fix[NG > 0 ? table_floats<NG, C>() : 1];
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   // the tables are built while each wave's first loads are in flight (for_each_group's prologue)
-  auto build = [&]() { build_tables<SPREAD>(tab, cf, k_base, K, n_groups, lr); };
-  const uint32_t lane_off = 4u * (threadIdx.x & 31u);  // the lane's copy of a spread table
+  auto build = [&]() { build_tables<C>(tab, cf, k_base, K, n_groups, lr); };
+  const uint32_t lane_off = 4u * (threadIdx.x % (C > 0 ? C : 32));  // the lane's copy of a spread table
   const uint32_t g_first = k_base / 8;
   constexpr int R = GroupShape<S>::kRows;
   // two groups in flight for the table counts that stream at one or two workgroups per CU;
   // one for the heavier updates, which run more waves per CU
-  constexpr int kAhead = NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
+  constexpr int kAhead = C > 0 || NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
   const bool restore_in_last = NG > 0 && r.group == g_first + static_cast<uint32_t>(NG) - 1;  // uniform
   for_each_group<S, kAhead, N>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
     uint32_t Wr[R][S::kWords];  // the last group's words, then the restore probe's
-    group_sums<S, NG, SPREAD>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off, Wr);
+    group_sums<S, NG, C>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off, Wr);
     if (RESTORE && !restore_in_last) group_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
     for (int u = 0; u < R; ++u) {
@@ -718,7 +732,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
   }, build);
   for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
-    tile_sums<SPREAD>(acc, tab, gen, t, n_groups, g_first);
+    tile_sums<C>(acc, tab, gen, t, n_groups, g_first);
     const uint4 rr = RESTORE ? gen.block(t, r.group) : make_uint4(0, 0, 0, 0);
     const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
     tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
@@ -850,8 +864,9 @@ struct Sweep {
 // update needs more waves where its generator and table work per byte outgrows what one wave
 // overlaps with its own loads; the caps below are the fastest of 1-4 workgroups per CU and
 // full occupancy, 16 to 64 KiB chunks and one or two groups in flight, measured for every
-// kernel on OPT-13B shaped bf16 and 3 G-element fp32 buffers. Updates with more probe groups
-// (K >= 32 in bf16, K >= 56 in fp32) are bound by the generator or the LDS table lookups
+// kernel on OPT-13B shaped bf16 and 3 G-element fp32 buffers (four bf16 probe groups with
+// their 16-copy tables: on an OPT-30B shaped buffer). Updates with more probe groups
+// (K >= 40 in bf16, K >= 56 in fp32) are bound by the generator or the LDS table lookups
 // and keep 4 KiB chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity
 // Cache. Grids: up to kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of
 // many short-lived workgroups keeps the streams compact; a persistent grid of one workgroup
@@ -875,7 +890,7 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   if (w.update) {
     const uint32_t g = w.n_groups;
     if (elem == 2)
-      cap = g == 1 ? 1 : g == 2 ? (w.restore ? 2 : 1) : g == 3 ? 3 : 0;
+      cap = g == 1 ? 1 : g == 2 ? (w.restore ? 2 : 1) : g == 3 ? 3 : g == 4 ? 2 : 0;
     else
       cap = g <= 3 ? 1 : g == 4 ? 2 : g <= 6 ? 3 : 0;
   }
@@ -926,12 +941,23 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
     return;
   }
   const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
-  // spread tables where two groups (one in fp32) stream at a capped occupancy, the cases they
-  // measured faster (64 KiB per workgroup would limit an uncapped launch to two workgroups per
-  // CU; a single bf16 group leaves the shared table's LDS half idle and gains nothing)
-  const bool spread = cap > 0 && (w.n_groups == 2 || (w.n_groups == 1 && sizeof(typename S::storage) == 4));
+  // Copies of each table (64 KiB in all), where they measured faster: 32 for two groups (one in
+  // fp32) streaming at a capped occupancy (64 KiB per workgroup would limit an uncapped launch
+  // to two workgroups per CU; a single bf16 group leaves the shared table's LDS half idle and
+  // gains nothing); 16 for four bf16 groups at two workgroups per CU (OPT-30B K = 32: 23.6 ->
+  // 22.0 ms against shared tables at full occupancy; 32 copies, 128 KiB at one workgroup per
+  // CU, 26.1 ms, and 16 copies of eight groups at one per CU lost a third: four waves per CU
+  // cannot hide the generator and table latencies).
+  const bool bf16 = sizeof(typename S::storage) == 2;
+  uint32_t copies = 0;
+  if (cap > 0) {
+    if (w.n_groups == 2 || (w.n_groups == 1 && !bf16))
+      copies = 32;
+    else if (w.n_groups == 4 && bf16)
+      copies = 16;
+  }
   const size_t table_bytes =
-      spread ? size_t{kSpreadFloats} * sizeof(float) : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
+      copies ? size_t{kSpreadFloats} * sizeof(float) : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
   const size_t static_lds = fixed ? table_bytes : 0;
   const size_t pad = occupancy_lds(cap, static_lds);
   const size_t tables = fixed ? 0 : table_bytes;
@@ -943,11 +969,11 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
   auto dispatch = [&](auto restore) {
     constexpr bool R = decltype(restore)::value;
     switch (w.n_groups) {
-      case 1: spread ? go(update_kernel<S, 1, R, N, true>) : go(update_kernel<S, 1, R, N, false>); break;
-      case 2: spread ? go(update_kernel<S, 2, R, N, true>) : go(update_kernel<S, 2, R, N, false>); break;
-      case 4: go(update_kernel<S, 4, R, N, false>); break;
-      case 8: go(update_kernel<S, 8, R, N, false>); break;
-      default: go(update_kernel<S, 0, R, N, false>); break;
+      case 1: copies ? go(update_kernel<S, 1, R, N, 32>) : go(update_kernel<S, 1, R, N, 0>); break;
+      case 2: copies ? go(update_kernel<S, 2, R, N, 32>) : go(update_kernel<S, 2, R, N, 0>); break;
+      case 4: copies ? go(update_kernel<S, 4, R, N, 16>) : go(update_kernel<S, 4, R, N, 0>); break;
+      case 8: go(update_kernel<S, 8, R, N, 0>); break;
+      default: go(update_kernel<S, 0, R, N, 0>); break;
     }
   };
   if (w.restore)
