@@ -505,8 +505,9 @@ def test_segments_streaming_shape_equal_flat_bits():
     (tiny ones among multi-million ones, none a multiple of the 32 KiB chunk, the first at a
     global offset of 777) get, in every element, the bits that the single-buffer calls give
     the same values laid out flat: perturb, a two-probe transition, the update with restore at
-    K = 16 (streaming shape) and the update at K = 64 (short chunks). The single-buffer calls
-    are themselves checked against the oracle at full size."""
+    K = 16 (streaming shape, one chunk per wave), the update and the update with restore at
+    K = 32 (16-copy tables, two workgroups per CU) and the update at K = 64 (short chunks). The
+    single-buffer calls are themselves checked against the oracle at full size."""
     rng = np.random.default_rng(13)
     sizes = [int(x) for x in rng.integers(1, 8_000_000, 50)] + [1, 7, 1023, 1024, 1025, 16_385]
     sizes = [sizes[i] for i in rng.permutation(len(sizes))]
@@ -523,6 +524,7 @@ def test_segments_streaming_shape_equal_flat_bits():
     seed, step, eps, lr = 31, 4, 1e-3, 1e-3
     c16 = rng.standard_normal(16).astype(np.float32)
     c64 = rng.standard_normal(64).astype(np.float32)
+    c32 = rng.standard_normal(32).astype(np.float32)
 
     def same(what):
         torch.cuda.synchronize()
@@ -538,6 +540,12 @@ def test_segments_streaming_shape_equal_flat_bits():
     zo.zo_update_restore(flat, c16, lr, seed, step, 12, -eps, offset=base)
     zo.zo_update_segments(ts, offs, c16, lr, seed, step, 12, -eps)
     same("update_restore K=16")
+    zo.zo_update_ex(flat, c32, lr, seed, step, offset=base)
+    zo.zo_update_segments(ts, offs, c32, lr, seed, step)
+    same("update K=32")
+    zo.zo_update_restore(flat, c32, lr, seed, step, 31, -eps, offset=base)
+    zo.zo_update_segments(ts, offs, c32, lr, seed, step, 31, -eps)
+    same("update_restore K=32")
     zo.zo_update_ex(flat, c64, lr, seed, step, offset=base)
     zo.zo_update_segments(ts, offs, c64, lr, seed, step)
     same("update K=64")
