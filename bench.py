@@ -330,22 +330,37 @@ def main():
         if args.layout == "tensors":
             r["per_sweep"] = (f"one call covers {n_tensors} tensors in {-(-n_tensors // 64)} launches; "
                               "times are per call")
+        # VALU: issued lane-ops against the 2.4 GHz issue peak, and the measured busy share of
+        # the CUs' VALU issue capacity at the clock the GPU actually ran (SQ_ACTIVE_INST_VALU)
+        valu_busy = counters.get("valu_busy", {}).get(kernel)
+        ints = counters.get("int_instructions_per_launch", {}).get(kernel)
         if alu is not None:
             r["valu_tlaneops"] = round(alu, 2)
             r["alu_frac"] = round(alu / VALU_PEAK_TLANEOPS, 4)
+        if valu_busy is not None:
+            r["valu_busy"] = valu_busy
+        if ints is not None:
+            it = ints * 64 / (avg_ms * 1e-3) / 1e12
+            r["int32_int64_tlaneops"] = round(it, 2)
+            r["int32_int64_frac"] = round(it / VALU_PEAK_TLANEOPS, 4)
         lds = counters.get("lds_per_launch", {}).get(kernel)
+        lds_busy = lds["lds_busy"] if lds is not None and kernel == "zo_update" else None
         if kernel == "zo_update":
             # one table lookup per element and probe group
             glk = n * ((K + 7) // 8) / (avg_ms * 1e-3) / 1e9
             r["table_glookups_per_s"] = round(glk, 1)
-            if lds is not None:
-                r["lds_busy"] = lds["lds_busy"]
-                if lds["lds_busy"] > max(hbm_frac, r.get("alu_frac", 0.0)):
-                    r.update(bound="lds", achieved=round(glk, 1), peak=round(LDS_PEAK_GLOOKUPS, 1),
-                             unit="G lookups/s", frac=round(glk / LDS_PEAK_GLOOKUPS, 4),
-                             peak_random_index=round(LDS_RANDOM_GLOOKUPS, 1),
-                             frac_of_random_index_peak=round(glk / LDS_RANDOM_GLOOKUPS, 4))
-        if alu is not None and r["bound"] == "hbm" and alu / VALU_PEAK_TLANEOPS > hbm_frac:
+            if lds_busy is not None:
+                r["lds_busy"] = lds_busy
+        # the bound is the unit with the highest measured utilisation
+        valu_use = valu_busy if valu_busy is not None else r.get("alu_frac")
+        use = {"hbm": hbm_frac, "lds": lds_busy, "alu": valu_use}
+        bound = max((u for u in use if use[u] is not None), key=lambda u: use[u])
+        if bound == "lds":
+            r.update(bound="lds", achieved=round(glk, 1), peak=round(LDS_PEAK_GLOOKUPS, 1),
+                     unit="G lookups/s", frac=round(glk / LDS_PEAK_GLOOKUPS, 4),
+                     peak_random_index=round(LDS_RANDOM_GLOOKUPS, 1),
+                     frac_of_random_index_peak=round(glk / LDS_RANDOM_GLOOKUPS, 4))
+        elif bound == "alu":
             r.update(bound="alu", achieved=round(alu, 2), peak=round(VALU_PEAK_TLANEOPS, 2), unit="Tlane-op/s",
                      frac=round(alu / VALU_PEAK_TLANEOPS, 4))
         return r
