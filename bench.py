@@ -67,6 +67,13 @@ def measured_counters(workload, K, dtype, layout="flat"):
     return {}
 
 
+def binding_unit(hbm_frac, lds_busy=None, valu_busy=None):
+    """The unit that bounds a kernel: the highest of its HBM fraction, LDS busy share and VALU
+    busy share ("hbm", "lds" or "alu"); a share not measured (None) is left out."""
+    use = {"hbm": hbm_frac, "lds": lds_busy, "alu": valu_busy}
+    return max((u for u in use if use[u] is not None), key=lambda u: use[u])
+
+
 _CPU = {}
 
 
@@ -351,10 +358,7 @@ def main():
             r["table_glookups_per_s"] = round(glk, 1)
             if lds_busy is not None:
                 r["lds_busy"] = lds_busy
-        # the bound is the unit with the highest measured utilisation
-        valu_use = valu_busy if valu_busy is not None else r.get("alu_frac")
-        use = {"hbm": hbm_frac, "lds": lds_busy, "alu": valu_use}
-        bound = max((u for u in use if use[u] is not None), key=lambda u: use[u])
+        bound = binding_unit(hbm_frac, lds_busy, valu_busy if valu_busy is not None else r.get("alu_frac"))
         if bound == "lds":
             r.update(bound="lds", achieved=round(glk, 1), peak=round(LDS_PEAK_GLOOKUPS, 1),
                      unit="G lookups/s", frac=round(glk / LDS_PEAK_GLOOKUPS, 4),
