@@ -664,7 +664,7 @@ def _windows(n, rng, count, size, boundaries=()):
     return sorted({min(max(s, 0), n - 1) for s in starts})
 
 
-@pytest.mark.parametrize("name,K", [("opt125m", 16), ("opt13b", 16), ("opt1.3b", 64), ("opt30b", 32),
+@pytest.mark.parametrize("name,K", [("opt125m", 16), ("opt13b", 16), ("opt1.3b", 64), ("opt30b", 8), ("opt30b", 32),
                                     ("qwen3-1.7b", 60), ("qwen3-8b", 60)])
 def test_full_size_sampled_windows(name, K):
     """At the full OPT-shaped size, in the benchmark's launch configuration, on 32 random
