@@ -870,11 +870,13 @@ struct Sweep {
 // and keep 4 KiB chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity
 // Cache. Grids: up to kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of
 // many short-lived workgroups keeps the streams compact; a persistent grid of one workgroup
-// per CU measured 5.6 TB/s), except that the one-probe bf16 perturb, the one-group bf16
-// update and the two-group bf16 update with restore run one chunk per wave (OPT-13B: the
-// perturb 6.48 -> 6.67 TB/s, OPT-30B 6.20 -> 6.60; OPT-30B K = 8: the update 6.19 -> 6.53,
-// with restore 6.41 -> 6.70; OPT-13B K = 16, the update with restore 5.94 -> 6.13; the other
-// kernels measured equal or slower so, the K = 16 update 5.93 against 6.45 TB/s).
+// per CU measured 5.6 TB/s), except that the one-probe bf16 perturb, the two-probe fp32
+// perturb, the one-group bf16 update and the two-group bf16 update with restore run one chunk
+// per wave (OPT-13B: the perturb 6.48 -> 6.67 TB/s, OPT-30B 6.20 -> 6.60; 3 G fp32 weights:
+// the two-probe perturb 6.14 -> 6.22 in one probe group, 6.30 -> 6.48 across two; OPT-30B
+// K = 8: the update 6.19 -> 6.53, with restore 6.41 -> 6.70; OPT-13B K = 16, the update with
+// restore 5.94 -> 6.13; the other kernels measured equal or slower so, the K = 16 update 6.41
+// against 6.54 TB/s).
 struct Shape {
   uint32_t chunk_groups;
   uint32_t blocks_per_cu;    // 0: no cap
@@ -897,10 +899,11 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   }
   if (cap == 0) return short_chunks;
   const bool one_probe_bf16 = !w.update && !w.two && elem == 2;
+  const bool two_probes_fp32 = !w.update && w.two && elem == 4;
   const bool one_group_update_bf16 = w.update && w.n_groups == 1 && elem == 2;
   const bool restore_two_groups_bf16 = w.update && w.restore && w.n_groups == 2 && elem == 2;
   return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap,
-               one_probe_bf16 || one_group_update_bf16 || restore_two_groups_bf16 ? 1u : 0u};
+               one_probe_bf16 || two_probes_fp32 || one_group_update_bf16 || restore_two_groups_bf16 ? 1u : 0u};
 }
 
 // Dynamic LDS that, with `static_lds` bytes of the kernel's own, admits exactly `cap`
