@@ -211,3 +211,27 @@ def test_plain_c_consumer(tmp_path):
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0, r.stdout + r.stderr
     assert r.stdout.count("ok ") == 15 and "FAIL" not in r.stdout, r.stdout
+
+
+def test_missing_library_raises_and_nothing_falls_back():
+    """Without libzo.so every call raises ZoLibraryMissing (the host coefficient function
+    included); the package imports no other implementation of the method."""
+    code = (
+        "import sys\n"
+        "import paper_2609_38095_amd as zo\n"
+        "zo.LIB_PATH = '/nonexistent/libzo.so'\n"
+        "zo._LIB = None\n"
+        "calls = [zo.library, zo.zo_version, lambda: zo.zo_probe_coeffs([2.0], [2.0], 2.0, 1e-3),\n"
+        "         lambda: zo.zo_probe_coeffs_ex([2.0], [2.0], 2.0, 1e-3), lambda: zo.zo_set_max_blocks(0)]\n"
+        "for call in calls:\n"
+        "    try:\n"
+        "        call()\n"
+        "    except zo.ZoLibraryMissing:\n"
+        "        continue\n"
+        "    sys.exit('a call succeeded without the library')\n"
+        "assert 'oracle' not in sys.modules, 'the binding imported the oracle'\n"
+        "print('ok')\n")
+    r = subprocess.run([os.sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stderr
+    src = open(os.path.join(ROOT, "paper_2609_38095_amd", "__init__.py")).read()
+    assert not re.search(r"^\s*(from|import)\s+(oracle|\.\.oracle)", src, flags=re.M)
