@@ -202,9 +202,11 @@ int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_
 const char* zo_strerror(int status);
 
 /*
- * zo_set_max_blocks -- caps the number of workgroups per sweep launch (0 restores the
- * default). Results do not depend on it; it exists to check that and to tune launch
- * width. Process-wide; not synchronised with launches in flight on other threads.
+ * zo_set_max_blocks -- a test hook: caps the number of workgroups of every later sweep
+ * launch in the process (0 restores the default shapes), so that tests can check that
+ * results do not depend on the grid. Results never depend on it. The value is stored
+ * atomically (a launch on another thread sees the old or the new cap, never a mix), but it
+ * is process-wide: it changes the launches of every caller, on every stream, until reset.
  */
 void zo_set_max_blocks(uint32_t max_blocks);
 

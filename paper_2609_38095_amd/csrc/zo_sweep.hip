@@ -39,29 +39,21 @@
 
 #include <hip/hip_runtime.h>
 
-#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <type_traits>
-#include <utility>
-#include <vector>
 
 #include "zo.h"
+#include "zo_plan.h"
 
 namespace {
 
-constexpr uint32_t kTile = 16;    // elements per generator block
-constexpr uint32_t kBlock = 256;  // threads per workgroup (4 waves)
-constexpr uint32_t kWavesPerBlock = kBlock / 64;
+using namespace zo;
+
 // s_waitcnt immediate for vmcnt(n), n < 16, that leaves expcnt and lgkmcnt unconstrained
 // (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
 constexpr int wait_vmcnt(int n) { return 0x0F70 | n; }
-constexpr uint64_t kGroupElems = 1024;      // elements per row group (one Philox block per lane)
-constexpr uint64_t kMaxChunkBytes = 32768;  // bytes a wave streams per chunk, at most
-constexpr uint32_t kDefaultMaxBlocks = 65536;
 constexpr int kRounds = 10;
-
-uint32_t g_max_blocks = 0;  // 0: default
 
 // ---------------------------------------------------------------------------------------
 // Philox4x32-R: round (x0,x1,x2,x3) -> (hi(M1 x2)^x1^k0, lo(M1 x2), hi(M0 x0)^x3^k1, lo(M0 x0)),
@@ -90,12 +82,10 @@ __device__ __forceinline__ uint4 philox4x32(uint32_t x0, uint32_t x1, uint32_t x
   return make_uint4(x0, x1, x2, x3);
 }
 
-struct Gen {
-  uint32_t k0, k1, step;
-  __device__ __forceinline__ uint4 block(uint64_t t, uint32_t group) const {
-    return philox4x32(static_cast<uint32_t>(t), static_cast<uint32_t>(t >> 32), step, group, k0, k1);
-  }
-};
+// The block of tile t and probe group `group`: counter (t mod 2^32, t / 2^32, step, group).
+__device__ __forceinline__ uint4 gen_block(const Gen& gen, uint64_t t, uint32_t group) {
+  return philox4x32(static_cast<uint32_t>(t), static_cast<uint32_t>(t >> 32), gen.step, group, gen.k0, gen.k1);
+}
 
 // Byte e (0..3) of a generator word: the probe byte of one element.
 __device__ __forceinline__ uint32_t word_byte(uint32_t w, int e) { return (w >> (8 * e)) & 0xFFu; }
@@ -200,7 +190,7 @@ __device__ __forceinline__ uint32_t vec_of_lane(uint32_t lane) {
 __device__ __forceinline__ void group_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
                                             uint32_t (&W)[2][BF16::kWords], BF16) {
   const uint32_t q = lane >> 5, m = lane & 31u;
-  const uint4 r = gen.block(vbase / 2 + 32ull * q + m, group);
+  const uint4 r = gen_block(gen, vbase / 2 + 32ull * q + m, group);
   const auto sx = __builtin_amdgcn_permlane32_swap(r.x, r.z, false, false);
   const auto sy = __builtin_amdgcn_permlane32_swap(r.y, r.w, false, false);
   W[0][0] = sx[0];
@@ -216,7 +206,7 @@ __device__ __forceinline__ void group_words(const Gen& gen, uint64_t vbase, uint
 __device__ __forceinline__ void group_words(const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t group,
                                             uint32_t (&W)[4][F32::kWords], F32) {
   const uint32_t q = lane >> 4, m = lane & 15u;
-  const uint4 r = gen.block(vbase / 4 + 16ull * q + m, group);
+  const uint4 r = gen_block(gen, vbase / 4 + 16ull * q + m, group);
   uint32_t a[4] = {r.x, r.y, r.z, r.w};
   auto sw32 = [&](int i, int j) {
     const auto p = __builtin_amdgcn_permlane32_swap(a[i], a[j], false, false);
@@ -258,36 +248,6 @@ __device__ __forceinline__ void tile_elementwise(typename S::storage* params, ui
   }
 }
 
-// One segment: global elements [lo, hi) stored from `base` (the address of global element lo).
-// The `span` full row groups from global group g_lo (stored from `gbase`) take the vector
-// path, in chunks of up to `chunk_groups` groups aligned to multiples of chunk_groups in the
-// global group index: the segment's first chunk starts `head` = g_lo mod chunk_groups groups
-// before g_lo. The edge tiles [head_t0, +head_nt) and [tail_t0, +tail_nt) (fewer than 1024
-// elements at each end) take the element-wise path. The kernels walk chunks and groups with
-// 32-bit indices relative to the segment (compares of 64-bit indices need a vector register
-// on gfx950, and writing one that a pending store still reads makes the wave wait for that
-// store); the host keeps a segment below 2^30 row groups and a launch below 2^31 chunks.
-struct Plan {
-  char* base;
-  uint64_t lo, hi;
-  char* gbase;
-  uint64_t g_lo;
-  uint32_t head, span;
-  uint64_t head_t0, tail_t0;
-  uint32_t head_nt, tail_nt;
-};
-
-// The segments one launch covers. Their chunks and edge tiles are numbered consecutively:
-// segment s owns chunks [chunk_end[s-1], chunk_end[s]) and edge tiles [edge_end[s-1], edge_end[s]).
-template <int N>
-struct Plans {
-  uint32_t count;
-  uint32_t chunk_groups;
-  uint32_t chunk_end[N];
-  uint32_t edge_end[N];
-  Plan p[N];
-};
-
 // The first segment s in [from, count) with x < ends[s], where ends is nondecreasing and
 // x < ends[count - 1]: a binary search, so that finding a chunk's segment costs at most
 // log2(N) + 1 argument loads wherever the chunk lies.
@@ -319,60 +279,74 @@ __device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupSh
 }
 
 // Calls body(vbase, d, lane) for every full row group of the launch, where vbase is the
-// group's global vector index and d its data, and stores what the body leaves in d. One
-// wave per chunk walks the chunk's groups in address order with the loads of the next AHEAD
-// groups in flight while the body works on the current one (each wave streams up to 32 KiB,
-// reads and writes interleaved). A wave's chunk indices increase, so its segment cursor
-// only moves forward. PACE > 0 (two ahead only): each step of three groups first waits until
-// at most PACE memory operations of the wave are outstanding: with 2, only the step's own
-// prefetch; with 4, also the previous step's last stores. The lightest sweeps stream HBM
-// faster paced (OPT-13B bf16 perturb: 6.40 TB/s with every request the loop allows in
-// flight, 6.67 paced at 2, 6.76 at 4; pacing at 6 or 8 measured lower), heavier ones need
-// the overlap.
+// group's global vector index and d its data, and stores what the body leaves in d. Each
+// chunk is one stream walked in address order by WPS waves of a workgroup of BLOCK threads:
+// wave w of the stream takes the chunk's groups w, w + WPS, w + 2 WPS, ..., with the loads of
+// its next AHEAD groups in flight while the body works on the current one (a stream of up to
+// 32 KiB, reads and writes interleaved). More waves per stream give the generator and table
+// work more waves to hide behind without adding streams. A wave's chunk indices increase,
+// so its segment cursor only moves forward. PACE > 0 (two ahead only): each step of three
+// groups first waits until at most PACE memory operations of the wave are outstanding: with
+// 2, only the step's own prefetch; with 4, also the previous step's last stores. The
+// lightest sweeps stream HBM faster paced (OPT-13B bf16 perturb: 6.40 TB/s with every
+// request the loop allows in flight, 6.67 paced at 2, 6.76 at 4; pacing at 6 or 8 measured
+// lower), heavier ones need the overlap.
 // prologue() runs once per wave, after the loads of the wave's first group are issued (at
-// once for a wave without chunks), so that work such as building the update's LDS tables
+// once for a wave without groups), so that work such as building the update's LDS tables
 // overlaps their latency; it may hold a workgroup barrier, which every wave reaches once.
-template <class S, int AHEAD, int N, int PACE = 0, class Body, class Prologue>
+template <class S, int AHEAD, int N, int PACE = 0, int BLOCK = 256, int WPS = 1, class Body, class Prologue>
 __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Prologue prologue) {
-  static_assert(PACE == 0 || (AHEAD == 2 && PACE >= 2 && PACE < 16), "pacing applies to the two-ahead loop");
-  static_assert(AHEAD == 1 || AHEAD == 2, "one or two groups in flight");
+  static_assert(PACE == 0 || (AHEAD >= 2 && PACE >= 2 && PACE < 16), "pacing applies to the two- and three-ahead loops");
+  static_assert(AHEAD >= 1 && AHEAD <= 3, "one to three groups in flight");
+  static_assert(BLOCK % 64 == 0 && (WPS == 1 || WPS == 2 || WPS == 4) && (BLOCK / 64) % WPS == 0,
+                "whole streams per workgroup");
   using G = GroupShape<S>;
-  const uint32_t n_waves = gridDim.x * kWavesPerBlock;
+  constexpr uint32_t kStreams = BLOCK / 64 / WPS;  // streams per workgroup
+  constexpr uint64_t kStride = WPS * G::kBytes;    // bytes between one wave's groups
+  const uint32_t n_streams = gridDim.x * kStreams;
   const uint32_t total = ps.chunk_end[ps.count - 1];
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t sub = wave % WPS;
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t cg = ps.chunk_groups;
   uint32_t s = 0;
-  uint32_t c = blockIdx.x * kWavesPerBlock + wave;
+  uint32_t c = blockIdx.x * kStreams + wave / WPS;
   if (c >= total) prologue();
-  for (bool first = true; c < total; c += n_waves, first = false) {
+  for (bool first = true; c < total; c += n_streams, first = false) {
     if (c >= ps.chunk_end[s]) s = segment_of(ps.chunk_end, s + 1, ps.count, c);
     const Plan& pl = ps.p[s];
     // the chunk's groups [g0, g1), relative to the segment's first full group (a select on the
     // chunk index, not a clamped subtraction, which has no scalar form)
     const uint32_t j = c - (s ? ps.chunk_end[s - 1] : 0);
     const uint32_t end = (j + 1) * cg - pl.head;
-    const uint32_t g0 = j ? j * cg - pl.head : 0u;
+    const uint32_t g0 = (j ? j * cg - pl.head : 0u) + sub;  // this wave's first group
     const uint32_t g1 = end < pl.span ? end : pl.span;
+    if (g0 >= g1) {  // a short last chunk may leave a wave of its stream without a group
+      if (first) prologue();
+      continue;
+    }
+    const uint32_t cnt = (g1 - g0 + (WPS - 1)) / WPS;  // this wave's groups in the chunk
     const uint64_t g_base = pl.g_lo;
     char* base = pl.gbase + static_cast<uint64_t>(g0) * G::kBytes;
     // Rotating register sets: while the body works on one group, the loads of the next AHEAD
     // groups are in flight. No register of an outstanding load is ever copied, and inside the
     // loops the prefetches do not depend on a branch (either would make the compiler wait
     // for every outstanding load before the work).
-    u32x4 x[G::kRows], y[G::kRows], z[G::kRows];
-    auto work = [&](u32x4 (&cur)[G::kRows], uint32_t g) {
+    u32x4 x[G::kRows], y[G::kRows], z[G::kRows], v[G::kRows];
+    uint32_t g = g0, i = 0;  // the current group and its index among the wave's groups
+    auto work = [&](u32x4 (&cur)[G::kRows]) {
       body((g_base + g) * G::kVecs, cur, lane);
       store_group<S>(base, cur, lane);
-      base += G::kBytes;
+      base += kStride;
+      g += WPS;
+      ++i;
     };
     auto prefetch = [&](u32x4 (&nxt)[G::kRows], uint32_t ahead) {
-      load_group<S>(nxt, base + ahead * G::kBytes, lane);
+      load_group<S>(nxt, base + ahead * kStride, lane);
       __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the work (the scheduler sinks it)
     };
     load_group<S>(x, base, lane);
     if (first) prologue();
-    uint32_t g = g0;
     // Each steady-state loop is entered only after one full step of it has run (peeled), so
     // that the loop is entered with the same loads and stores outstanding as its back edge:
     // the compiler then waits for exactly the group a step needs. Entered straight from the
@@ -381,73 +355,130 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Pr
     if constexpr (AHEAD == 1) {
       auto step2 = [&]() {
         prefetch(y, 1);
-        work(x, g);
+        work(x);
         prefetch(x, 1);
-        work(y, g + 1);
-        g += 2;
+        work(y);
       };
-      if (g + 2 < g1) {  // at least three groups left: steps of two that both prefetch
+      if (i + 2 < cnt) {  // at least three groups left: steps of two that both prefetch
         step2();
-        while (g + 2 < g1) step2();
+        while (i + 2 < cnt) step2();
       }
-      if (g + 1 < g1) {  // two groups left
+      if (i + 1 < cnt) {  // two groups left
         prefetch(y, 1);
-        work(x, g);
-        work(y, g + 1);
+        work(x);
+        work(y);
       } else {
-        work(x, g);
+        work(x);
       }
-    } else {
+    } else if constexpr (AHEAD == 2) {
       auto step3 = [&]() {
         prefetch(z, 2);
         if constexpr (PACE > 0) __builtin_amdgcn_s_waitcnt(wait_vmcnt(PACE));
-        work(x, g);
+        work(x);
         prefetch(x, 2);
-        work(y, g + 1);
+        work(y);
         prefetch(y, 2);
-        work(z, g + 2);
-        g += 3;
+        work(z);
       };
       // 2 to 4 groups left, x and y requested
       auto last = [&]() {
-        if (g + 2 < g1) {
+        if (i + 2 < cnt) {
           prefetch(z, 2);
-          work(x, g);
-          if (g + 3 < g1) {
+          work(x);
+          if (i + 2 < cnt) {
             prefetch(x, 2);
-            work(y, g + 1);
-            work(z, g + 2);
-            work(x, g + 3);
+            work(y);
+            work(z);
+            work(x);
           } else {
-            work(y, g + 1);
-            work(z, g + 2);
+            work(y);
+            work(z);
           }
         } else {
-          work(x, g);
-          work(y, g + 1);
+          work(x);
+          work(y);
         }
       };
-      if (g + 4 < g1) {  // at least five groups left: steps of three that prefetch two ahead
-        load_group<S>(y, base + G::kBytes, lane);
+      if (i + 4 < cnt) {  // at least five groups left: steps of three that prefetch two ahead
+        load_group<S>(y, base + kStride, lane);
         step3();
-        while (g + 4 < g1) step3();
+        while (i + 4 < cnt) step3();
         last();
-      } else if (g + 1 < g1) {
-        load_group<S>(y, base + G::kBytes, lane);
+      } else if (i + 1 < cnt) {
+        load_group<S>(y, base + kStride, lane);
         last();
       } else {
-        work(x, g);
+        work(x);
+      }
+    } else {
+      auto step4 = [&]() {
+        prefetch(v, 3);
+        if constexpr (PACE > 0) __builtin_amdgcn_s_waitcnt(wait_vmcnt(PACE));
+        work(x);
+        prefetch(x, 3);
+        work(y);
+        prefetch(y, 3);
+        work(z);
+        prefetch(z, 3);
+        work(v);
+      };
+      // 3 to 6 groups left, x, y and z requested
+      auto last = [&]() {
+        if (i + 3 < cnt) {
+          prefetch(v, 3);
+          work(x);
+          if (i + 3 < cnt) {
+            prefetch(x, 3);
+            work(y);
+            if (i + 3 < cnt) {
+              prefetch(y, 3);
+              work(z);
+              work(v);
+              work(x);
+              work(y);
+            } else {
+              work(z);
+              work(v);
+              work(x);
+            }
+          } else {
+            work(y);
+            work(z);
+            work(v);
+          }
+        } else {
+          work(x);
+          work(y);
+          work(z);
+        }
+      };
+      if (i + 6 < cnt) {  // at least seven groups left: steps of four that prefetch three ahead
+        load_group<S>(y, base + kStride, lane);
+        load_group<S>(z, base + 2 * kStride, lane);
+        step4();
+        while (i + 6 < cnt) step4();
+        last();
+      } else if (i + 2 < cnt) {
+        load_group<S>(y, base + kStride, lane);
+        load_group<S>(z, base + 2 * kStride, lane);
+        last();
+      } else if (i + 1 < cnt) {
+        load_group<S>(y, base + kStride, lane);
+        work(x);
+        work(y);
+      } else {
+        work(x);
       }
     }
   }
 }
 
 // Calls body(plan, tile) for every edge tile of the launch, one lane per tile.
-template <int N, class Body>
+template <int N, int BLOCK, class Body>
 __device__ __forceinline__ void for_each_edge(const Plans<N>& ps, Body body) {
   const uint32_t n_edge = ps.edge_end[ps.count - 1];
-  const uint32_t stride = gridDim.x * kBlock;
-  for (uint32_t j = blockIdx.x * kBlock + threadIdx.x; j < n_edge; j += stride) {
+  const uint32_t stride = gridDim.x * BLOCK;
+  for (uint32_t j = blockIdx.x * BLOCK + threadIdx.x; j < n_edge; j += stride) {
     const uint32_t s = segment_of(ps.edge_end, 0, ps.count, j);
     const Plan& pl = ps.p[s];
     const uint32_t lj = j - (s ? ps.edge_end[s - 1] : 0);
@@ -458,20 +489,16 @@ __device__ __forceinline__ void for_each_edge(const Plans<N>& ps, Body body) {
 // ---------------------------------------------------------------------------------------
 // perturb: theta + eps * z_k (bit k mod 8 of each probe byte of group k / 8). TWO: the
 // fused transition theta + (eps_a z_a + eps_b z_b), the pair's sum rounded to fp32 first.
-struct Probe {
-  uint32_t group, bit;
-  float eps;
-  __device__ __forceinline__ float delta(uint32_t byte) const { return ((byte >> bit) & 1u) ? eps : -eps; }
-};
+__device__ __forceinline__ float delta(const Probe& p, uint32_t byte) { return ((byte >> p.bit) & 1u) ? p.eps : -p.eps; }
 
-template <class S, bool TWO, int N, int PACE>
-__global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, Probe a, Probe b) {
+template <class S, bool TWO, int N, int PACE, int BLOCK, int WPS>
+__global__ __launch_bounds__(BLOCK) void perturb_kernel(Plans<N> ps, Gen gen, Probe a, Probe b) {
   extern __shared__ uint32_t occupancy_pad[];  // dynamic LDS only limits workgroups per CU
   if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count <= 64)
   constexpr int R = GroupShape<S>::kRows;
   const bool shared_group = a.group == b.group;
   auto no_prologue = []() {};
-  for_each_group<S, 2, N, PACE>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+  for_each_group<S, 2, N, PACE, BLOCK, WPS>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     uint32_t Wa[R][S::kWords], Wb[R][S::kWords];
     group_words(gen, vbase, lane, a.group, Wa, S());
     if (TWO) {
@@ -490,20 +517,20 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
       S::unpack(d[u], v);
 #pragma unroll
       for (int e = 0; e < S::kVecElems; ++e) {
-        float dv = a.delta(elem_byte<S>(Wa[u], e));
-        if (TWO) dv = dv + b.delta(elem_byte<S>(Wb[u], e));
+        float dv = delta(a, elem_byte<S>(Wa[u], e));
+        if (TWO) dv = dv + delta(b, elem_byte<S>(Wb[u], e));
         v[e] = v[e] + dv;
       }
       d[u] = S::pack(v);
     }
   }, no_prologue);
-  for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
-    const uint4 ra = gen.block(t, a.group);
-    const uint4 rb = TWO ? gen.block(t, b.group) : ra;
+  for_each_edge<N, BLOCK>(ps, [&](const Plan& pl, uint64_t t) {
+    const uint4 ra = gen_block(gen, t, a.group);
+    const uint4 rb = TWO ? gen_block(gen, t, b.group) : ra;
     const uint32_t xa[4] = {ra.x, ra.y, ra.z, ra.w}, xb[4] = {rb.x, rb.y, rb.z, rb.w};
     tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
-      float dv = a.delta(word_byte(xa[e >> 2], e & 3));
-      if (TWO) dv = dv + b.delta(word_byte(xb[e >> 2], e & 3));
+      float dv = delta(a, word_byte(xa[e >> 2], e & 3));
+      if (TWO) dv = dv + delta(b, word_byte(xb[e >> 2], e & 3));
       return v + dv;
     });
   });
@@ -511,24 +538,27 @@ __global__ __launch_bounds__(kBlock) void perturb_kernel(Plans<N> ps, Gen gen, P
 
 // ---------------------------------------------------------------------------------------
 // update: theta - lr * sum_k c_k z_k.
-struct Coefs {
-  float c[ZO_K_MAX];
-};
 
-// Spread tables, for streaming launches: C = 32 or 16 copies of each 256-entry table of up to
-// 64 / C groups (64 KiB), interleaved so that copy r of entry e of group g is float
-// 64 e + C g + r. Lane l reads copy l mod C, which sits in LDS bank (C g + l mod C) mod 32:
-// with 32 copies every lane of a half-wave has its own bank, so a 64-lane read of random
-// bytes takes 2 LDS cycles instead of about 6.3 when all lanes share one copy; with 16 copies
-// two lanes share a bank, about 4 cycles. A lookup's byte address, 256 e + 4 (l mod C) + 4 C g,
-// is one byte permute of the generator word and the lane's copy offset (as many instructions
-// as a lookup into a shared table).
-constexpr uint32_t kSpreadFloats = 256 * 64;
+// Spread tables, for streaming launches: C = 32 or 16 copies of each 256-entry table,
+// interleaved in planes of 64 KiB that hold P = 64 / C groups each (at most two planes): copy
+// r of entry e of group g is float 16384 (g / P) + 64 e + C (g mod P) + r. Lane l reads copy
+// l mod C, which sits in LDS bank (C (g mod P) + l mod C) mod 32: with 32 copies every lane of
+// a half-wave has its own bank, so a 64-lane read of random bytes takes 2 LDS cycles instead
+// of about 6.3 when all lanes share one copy; with 16 copies two lanes share a bank, about 4
+// cycles. A lookup's byte address, 65536 (g / P) + 256 e + 4 (l mod C) + 4 C (g mod P), is one
+// byte permute of the generator word and the lane's offset word (byte 0: 4 (l mod C), byte 2:
+// 1, selected for the second plane), plus an immediate offset: as many instructions as a
+// lookup into a shared table.
+constexpr uint32_t kSpreadFloats = 256 * 64;  // one plane
+template <int C>
+constexpr uint32_t groups_per_plane() {
+  return C > 0 ? 64 / C : 1;
+}
 // floats of the tables of NG groups: C interleaved copies, or one shared copy (C = 0)
 template <int NG, int C>
 constexpr uint32_t table_floats() {
-  static_assert(C == 0 || (C == 16 || C == 32) && NG * C <= 64, "spread tables fill at most 64 KiB");
-  return C == 0 ? NG * 256 : kSpreadFloats;
+  static_assert(C == 0 || ((C == 16 || C == 32) && NG * C <= 128), "spread tables fill at most two planes");
+  return C == 0 ? NG * 256 : (NG * C <= 64 ? 1 : 2) * kSpreadFloats;
 }
 
 // Build the n_groups x 256 table in LDS (C > 0: the interleaved copies). Entry (g, b):
@@ -537,17 +567,18 @@ constexpr uint32_t table_floats() {
 // multiply per element; with one probe the entry is +-fl(lr * c), the step a perturb by
 // -fl(lr * c) would apply. Thread b writes entry b of every group: the group loop and the
 // coefficient reads are uniform (scalar loads), and the sign of slot s is an XOR of the
-// coefficient's sign bit with bit s of ~b.
-static_assert(kBlock == 256, "one table entry per thread");
-template <int C>
+// coefficient's sign bit with bit s of ~b. A workgroup of BLOCK threads builds BLOCK / 256
+// groups at a time: thread b + 256 m writes entry b of groups m, m + BLOCK / 256, ...
+template <int C, int BLOCK>
 __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
                                              uint32_t n_groups, float lr) {
-  const uint32_t b = threadIdx.x;
+  static_assert(BLOCK % 256 == 0, "one table entry per thread");
+  const uint32_t b = threadIdx.x & 255u;
   uint32_t flip[8];
 #pragma unroll
   for (int s = 0; s < 8; ++s) flip[s] = ((~b) << (31 - s)) & 0x80000000u;
   const uint32_t g_first = k_base / 8;
-  for (uint32_t g = 0; g < n_groups; ++g) {
+  for (uint32_t g = threadIdx.x >> 8; g < n_groups; g += BLOCK / 256) {
     float v[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -560,8 +591,8 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
       // entry b's C / 4 float4 of copies, 256 bytes after entry b - 1's: thread b writes them
       // starting at float4 b mod (C / 4), so that the lanes of each write spread over the banks
       // the group's copies occupy (in a fixed order all 64 would land on the same 4 banks)
-      constexpr uint32_t Q = C / 4;
-      float* e = tab + 64u * b + C * g;
+      constexpr uint32_t Q = C / 4, P = groups_per_plane<C>();
+      float* e = tab + kSpreadFloats * (g / P) + 64u * b + C * (g % P);
       const float4 t4 = make_float4(t, t, t, t);
 #pragma unroll
       for (uint32_t q = 0; q < Q; ++q) *reinterpret_cast<float4*>(e + 4u * ((q + b) & (Q - 1))) = t4;
@@ -573,12 +604,16 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
 }
 
 // Spread-table lookup in group g (C copies): one byte permute forms the address (byte 0: the
-// lane's copy offset `lane_off` = 4 (l mod C), byte 1: byte e of w, upper bytes 0), then the
-// float there plus the group's offset 4 C g.
+// lane's copy offset, byte 0 of `lane_off` = 4 (l mod C); byte 1: byte e of w; byte 2: 0, or
+// for the second plane byte 2 of lane_off, which is 1; byte 3: 0), then the float there plus
+// the group's offset 4 C (g mod P) inside its plane.
 template <int C>
 __device__ __forceinline__ float spread_at(const float* tab, uint32_t lane_off, uint32_t w, int e, uint32_t g) {
-  const uint32_t addr = __builtin_amdgcn_perm(w, lane_off, 0x0C0C0000u | ((4u + static_cast<uint32_t>(e)) << 8));
-  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + addr + 4u * C * g);
+  constexpr uint32_t P = groups_per_plane<C>();
+  const uint32_t plane_sel = g / P ? 0x00020000u : 0x000C0000u;
+  const uint32_t addr =
+      __builtin_amdgcn_perm(w, lane_off, 0x0C000000u | plane_sel | ((4u + static_cast<uint32_t>(e)) << 8));
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + addr + 4u * C * (g % P));
 }
 
 // acc[u][e] (+)= table value of probe group g for each element of the row group; W receives
@@ -658,14 +693,15 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
     float part[kTile];
     const uint32_t g1 = n_groups - g0 < 8 ? n_groups : g0 + 8;
     for (uint32_t g = g0; g < g1; ++g) {
-      const uint4 r = gen.block(t, g_first + g);
+      const uint4 r = gen_block(gen, t, g_first + g);
       const uint32_t x[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
       for (int j = 0; j < (int)kTile; ++j) {
         const uint32_t byte = word_byte(x[j >> 2], j & 3);
         float v;
         if constexpr (C > 0) {
-          v = tab[64u * byte + C * g + (threadIdx.x % C)];
+          constexpr uint32_t P = groups_per_plane<C>();
+          v = tab[kSpreadFloats * (g / P) + 64u * byte + C * (g % P) + (threadIdx.x % C)];
         } else {
           v = tab[256u * g + byte];
         }
@@ -696,24 +732,25 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
 // step's last probe), its generator words are those the group sum has just produced; otherwise
 // they are generated after the group loop (keeping a middle group's words would hold them live
 // across the rest of it).
-template <class S, int NG, bool RESTORE, int N, int C>
-__global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
-                                                       uint32_t n_groups, Coefs cf, float lr, Probe r) {
+template <class S, int NG, bool RESTORE, int N, int C, int BLOCK, int WPS, int PACE = 0, int AHEAD = 0>
+__global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
+                                                      uint32_t n_groups, Coefs cf, float lr, Probe r) {
   // n_groups x 256 floats (C > 0: the interleaved copies): static for a fixed group count
   // (constant LDS offsets), else dynamic.
   extern __shared__ float tab_dyn[];
   __shared__ float tab_fix[NG > 0 ? table_floats<NG, C>() : 1];
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   // the tables are built while each wave's first loads are in flight (for_each_group's prologue)
-  auto build = [&]() { build_tables<C>(tab, cf, k_base, K, n_groups, lr); };
-  const uint32_t lane_off = 4u * (threadIdx.x % (C > 0 ? C : 32));  // the lane's copy of a spread table
+  auto build = [&]() { build_tables<C, BLOCK>(tab, cf, k_base, K, n_groups, lr); };
+  // the lane's copy of a spread table (byte 0) and the second plane's offset (byte 2)
+  const uint32_t lane_off = 4u * (threadIdx.x % (C > 0 ? C : 32)) | (1u << 16);
   const uint32_t g_first = k_base / 8;
   constexpr int R = GroupShape<S>::kRows;
   // two groups in flight for the table counts that stream at one or two workgroups per CU;
-  // one for the heavier updates, which run more waves per CU
-  constexpr int kAhead = C > 0 || NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
+  // one for the heavier updates, which run more waves per CU (AHEAD > 0 sets it)
+  constexpr int kAhead = AHEAD ? AHEAD : C > 0 || NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
   const bool restore_in_last = NG > 0 && r.group == g_first + static_cast<uint32_t>(NG) - 1;  // uniform
-  for_each_group<S, kAhead, N>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
+  for_each_group<S, kAhead, N, PACE, BLOCK, WPS>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
     uint32_t Wr[R][S::kWords];  // the last group's words, then the restore probe's
     group_sums<S, NG, C>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off, Wr);
@@ -724,19 +761,19 @@ __global__ __launch_bounds__(kBlock) void update_kernel(Plans<N> ps, Gen gen, ui
       S::unpack(d[u], v);
 #pragma unroll
       for (int e = 0; e < S::kVecElems; ++e) {
-        if (RESTORE) v[e] = v[e] + r.delta(elem_byte<S>(Wr[u], e));
+        if (RESTORE) v[e] = v[e] + delta(r, elem_byte<S>(Wr[u], e));
         v[e] = v[e] - acc[u][e];
       }
       d[u] = S::pack(v);
     }
   }, build);
-  for_each_edge(ps, [&](const Plan& pl, uint64_t t) {
+  for_each_edge<N, BLOCK>(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
     tile_sums<C>(acc, tab, gen, t, n_groups, g_first);
-    const uint4 rr = RESTORE ? gen.block(t, r.group) : make_uint4(0, 0, 0, 0);
+    const uint4 rr = RESTORE ? gen_block(gen, t, r.group) : make_uint4(0, 0, 0, 0);
     const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
     tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
-      if (RESTORE) v = v + r.delta(word_byte(xr[e >> 2], e & 3));
+      if (RESTORE) v = v + delta(r, word_byte(xr[e >> 2], e & 3));
       return v - acc[e];
     });
   });
@@ -747,172 +784,14 @@ __global__ __launch_bounds__(kBlock) void gen_bits_kernel(uint8_t* out, uint64_t
                                                          uint32_t group, Gen gen) {
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
   for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n_tiles; i += stride) {
-    const uint4 r = gen.block(tile_begin + i, group);
+    const uint4 r = gen_block(gen, tile_begin + i, group);
     *reinterpret_cast<u32x4*>(out + 16 * i) = u32x4{r.x, r.y, r.z, r.w};
   }
 }
 
 // ---------------------------------------------------------------------------------------
 // Host side.
-constexpr int kSegsPerLaunch = 64;                 // segments per batched launch (kernel arguments, ~5 KiB)
-constexpr uint64_t kMaxLaunchChunks = 1ull << 31;  // chunks per launch: 32-bit indices with room for the stride
-
-// The grid's cap: zo_set_max_blocks if set, else kDefaultMaxBlocks, or (sized) none: the
-// caller then sized work_items per workgroup itself.
-uint32_t cap_blocks(bool sized = false) { return g_max_blocks ? g_max_blocks : sized ? (1u << 30) : kDefaultMaxBlocks; }
-
-uint32_t grid_for(uint64_t work_items, uint64_t per_block, bool sized = false) {
-  const uint64_t need = (work_items + per_block - 1) / per_block;
-  const uint64_t cap = cap_blocks(sized);
-  const uint64_t g = need < cap ? need : cap;
-  return static_cast<uint32_t>(g ? g : 1);
-}
-
-int check_params(const void* params, zo_dtype dt, uint64_t offset, uint64_t n) {
-  if (dt != ZO_F32 && dt != ZO_BF16) return ZO_ERR_ARG;
-  if (n == 0) return ZO_OK;
-  if (params == nullptr) return ZO_ERR_NULL;
-  if (reinterpret_cast<uintptr_t>(params) % (dt == ZO_F32 ? 4 : 2) != 0) return ZO_ERR_ARG;
-  if (offset + n < offset || offset + n == 0) return ZO_ERR_ARG;  // reaches 2^64
-  if (n >= ZO_N_MAX) return ZO_ERR_ARG;  // more weights than a device holds
-  return ZO_OK;
-}
-
-uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
-
-// Full row groups need the address of global element 0 (params shifted back by offset
-// elements) to be 16-byte aligned, so that every group vector is an aligned 16 bytes.
-Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint32_t chunk_groups) {
-  Plan pl{};
-  pl.base = static_cast<char*>(params);
-  pl.lo = offset;
-  pl.hi = offset + n;
-  if (n == 0) return pl;
-  const uintptr_t base = reinterpret_cast<uintptr_t>(params) - static_cast<uintptr_t>(offset * elem);
-  uint64_t head_end = pl.hi, tail_begin = pl.hi;
-  if ((base & 15u) == 0) {
-    const uint64_t g_lo = ceil_div(pl.lo, kGroupElems), g_hi = pl.hi / kGroupElems;
-    if (g_lo < g_hi) {  // g_hi - g_lo < 2^30: n < ZO_N_MAX is checked first
-      pl.g_lo = g_lo;
-      pl.span = static_cast<uint32_t>(g_hi - g_lo);
-      pl.head = static_cast<uint32_t>(g_lo % chunk_groups);
-      pl.gbase = pl.base + (g_lo * kGroupElems - pl.lo) * elem;
-      head_end = g_lo * kGroupElems;
-      tail_begin = g_hi * kGroupElems;
-    }
-  }
-  if (head_end > pl.lo) {
-    pl.head_t0 = pl.lo / kTile;
-    pl.head_nt = static_cast<uint32_t>(ceil_div(head_end, kTile) - pl.head_t0);
-  }
-  if (pl.hi > tail_begin) {
-    pl.tail_t0 = tail_begin / kTile;
-    pl.tail_nt = static_cast<uint32_t>(ceil_div(pl.hi, kTile) - pl.tail_t0);
-  }
-  return pl;
-}
-
-// Chunks that meet a plan's full row groups (fewer than 2^30 + 2).
-uint32_t plan_chunks(const Plan& pl, uint32_t chunk_groups) {
-  return pl.span ? static_cast<uint32_t>(ceil_div(static_cast<uint64_t>(pl.head) + pl.span, chunk_groups)) : 0u;
-}
-
-template <int N>
-void add_plan(Plans<N>& ps, const Plan& pl) {
-  const uint32_t s = ps.count++;
-  ps.p[s] = pl;
-  ps.chunk_end[s] = (s ? ps.chunk_end[s - 1] : 0) + plan_chunks(pl, ps.chunk_groups);
-  ps.edge_end[s] = (s ? ps.edge_end[s - 1] : 0) + pl.head_nt + pl.tail_nt;
-}
-
-// chunks_per_wave > 0: one workgroup per kWavesPerBlock * chunks_per_wave chunks; 0: up to
-// kDefaultMaxBlocks workgroups, grid-stride beyond.
-template <int N>
-uint32_t plans_grid(const Plans<N>& ps, uint32_t chunks_per_wave) {
-  const uint32_t chunks = ps.chunk_end[ps.count - 1], edges = ps.edge_end[ps.count - 1];
-  const uint32_t a =
-      chunks ? grid_for(chunks, uint64_t{kWavesPerBlock} * (chunks_per_wave ? chunks_per_wave : 1), chunks_per_wave > 0) : 1;
-  const uint32_t b = grid_for(edges, kBlock);
-  return a > b ? a : b;
-}
-
 int launch_status() { return hipGetLastError() == hipSuccess ? ZO_OK : ZO_ERR_HIP; }
-
-Probe make_probe(uint32_t k, float eps) { return Probe{k / 8, k % 8, eps}; }
-
-Gen make_gen(uint64_t seed, uint32_t step) {
-  return Gen{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), step};
-}
-
-// What one sweep applies: one or two probes, or the update (with an optional restore probe).
-struct Sweep {
-  bool update;
-  Probe a, b;
-  bool two;
-  uint32_t k_base, K, n_groups;
-  Coefs cf;
-  float lr;
-  Probe r;
-  bool restore;
-};
-
-// Streaming shape of a launch over `elements` weights of `elem` bytes. HBM sustains these
-// in-place sweeps best as few long sequential read-write streams: each wave walks up to
-// kMaxChunkBytes of consecutive row groups with the next one or two groups in flight, and
-// occupancy is capped with dynamic LDS so that few waves stream at once (the bf16 perturb on
-// an OPT-13B shaped buffer: 6.5 TB/s at one workgroup per CU, 5.6 at full occupancy). An
-// update needs more waves where its generator and table work per byte outgrows what one wave
-// overlaps with its own loads; the caps below are the fastest of 1-4 workgroups per CU and
-// full occupancy, 16 to 64 KiB chunks and one or two groups in flight, measured for every
-// kernel on OPT-13B shaped bf16 and 3 G-element fp32 buffers (four bf16 probe groups with
-// their 16-copy tables: on an OPT-30B shaped buffer). Updates with more probe groups
-// (K >= 40 in bf16, K >= 56 in fp32) are bound by the generator or the LDS table lookups
-// and keep 4 KiB chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity
-// Cache. Grids: up to kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of
-// many short-lived workgroups keeps the streams compact; a persistent grid of one workgroup
-// per CU measured 5.6 TB/s), except that the one-probe bf16 perturb, the two-probe fp32
-// perturb, the one-group bf16 update and the two-group bf16 update with restore run one chunk
-// per wave (OPT-13B: the perturb 6.48 -> 6.67 TB/s, OPT-30B 6.20 -> 6.60; 3 G fp32 weights:
-// the two-probe perturb 6.14 -> 6.22 in one probe group, 6.30 -> 6.48 across two; OPT-30B
-// K = 8: the update 6.19 -> 6.53, with restore 6.41 -> 6.70; OPT-13B K = 16, the update with
-// restore 5.94 -> 6.13; the other kernels measured equal or slower so, the K = 16 update 6.41
-// against 6.54 TB/s).
-struct Shape {
-  uint32_t chunk_groups;
-  uint32_t blocks_per_cu;    // 0: no cap
-  uint32_t chunks_per_wave;  // 0: up to kDefaultMaxBlocks workgroups, grid-stride beyond
-};
-
-constexpr uint64_t kStreamBytes = 256ull << 20;
-
-Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
-  const uint64_t group_bytes = kGroupElems * elem;
-  const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0, 0};
-  if (elements * elem < kStreamBytes) return short_chunks;
-  uint32_t cap = 1;  // the perturb kernels, one or two probes
-  if (w.update) {
-    const uint32_t g = w.n_groups;
-    if (elem == 2)
-      cap = g == 1 ? 1 : g == 2 ? (w.restore ? 2 : 1) : g == 3 ? 3 : g == 4 ? 2 : 0;
-    else
-      cap = g <= 3 ? 1 : g == 4 ? 2 : g <= 6 ? 3 : 0;
-  }
-  if (cap == 0) return short_chunks;
-  const bool one_probe_bf16 = !w.update && !w.two && elem == 2;
-  const bool two_probes_fp32 = !w.update && w.two && elem == 4;
-  const bool one_group_update_bf16 = w.update && w.n_groups == 1 && elem == 2;
-  const bool restore_two_groups_bf16 = w.update && w.restore && w.n_groups == 2 && elem == 2;
-  return Shape{static_cast<uint32_t>(kMaxChunkBytes / group_bytes), cap,
-               one_probe_bf16 || two_probes_fp32 || one_group_update_bf16 || restore_two_groups_bf16 ? 1u : 0u};
-}
-
-// Dynamic LDS that, with `static_lds` bytes of the kernel's own, admits exactly `cap`
-// workgroups on a CU's 160 KiB (0: no cap).
-size_t occupancy_lds(uint32_t cap, size_t static_lds) {
-  if (cap == 0) return 0;
-  const size_t per_block = cap == 1 ? 96 * 1024 : cap == 2 ? 72 * 1024 : cap == 3 ? 48 * 1024 : 36 * 1024;
-  return per_block > static_lds ? per_block - static_lds : 0;
-}
 
 // A workgroup's LDS above 64 KiB (static plus dynamic) must be allowed per kernel before the
 // launch.
@@ -923,15 +802,28 @@ void allow_lds(K kernel, size_t dynamic_bytes, size_t static_bytes = 0) {
                               static_cast<int>(dynamic_bytes));
 }
 
+// Launch dimensions a kernel is built for: workgroup size and waves per stream. A kernel is
+// always launched with the dimensions it was built for.
+template <int B, int W>
+struct Dims {
+  static constexpr int block = B, wps = W;
+};
+
 template <class S, int N>
 void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shape& sh, hipStream_t st) {
   const uint32_t cap = sh.blocks_per_cu;
-  const dim3 grid(plans_grid(ps, sh.chunks_per_wave)), block(kBlock);
+  // the grid of a launch with B threads per workgroup and W waves per stream
+  auto grid_of = [&](uint32_t B, uint32_t W) {
+    Shape s = sh;
+    s.block = B;
+    s.wps = W;
+    return dim3(plans_grid(ps, s));
+  };
   if (!w.update) {
     const size_t pad = occupancy_lds(cap, 0);
     auto go = [&](auto kernel, Probe b) {
       allow_lds(kernel, pad);
-      kernel<<<grid, block, pad, st>>>(ps, gen, w.a, b);
+      kernel<<<grid_of(kBlock, 1), dim3(kBlock), pad, st>>>(ps, gen, w.a, b);
     };
     // paced when the generator work per byte is lightest: one probe group, or fp32 with two;
     // bf16 at 4 outstanding operations (one probe +1.3%, two in one group +3.4% over 2), fp32
@@ -940,45 +832,77 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
     const bool two_groups = w.two && w.a.group != w.b.group;
     const bool paced = (two_groups ? 2u : 1u) * (sizeof(typename S::storage) == 2 ? 2u : 1u) <= 2u;
     if (w.two)
-      paced ? go(perturb_kernel<S, true, N, kPace>, w.b) : go(perturb_kernel<S, true, N, 0>, w.b);
+      paced ? go(perturb_kernel<S, true, N, kPace, kBlock, 1>, w.b) : go(perturb_kernel<S, true, N, 0, kBlock, 1>, w.b);
     else
-      paced ? go(perturb_kernel<S, false, N, kPace>, w.a) : go(perturb_kernel<S, false, N, 0>, w.a);
+      paced ? go(perturb_kernel<S, false, N, kPace, kBlock, 1>, w.a) : go(perturb_kernel<S, false, N, 0, kBlock, 1>, w.a);
     return;
   }
-  const bool fixed = w.n_groups == 1 || w.n_groups == 2 || w.n_groups == 4 || w.n_groups == 8;
-  // Copies of each table (64 KiB in all), where they measured faster: 32 for two groups (one in
-  // fp32) streaming at a capped occupancy (64 KiB per workgroup would limit an uncapped launch
-  // to two workgroups per CU; a single bf16 group leaves the shared table's LDS half idle and
-  // gains nothing); 16 for four bf16 groups at two workgroups per CU (OPT-30B K = 32: 23.6 ->
-  // 22.0 ms against shared tables at full occupancy; 32 copies, 128 KiB at one workgroup per
-  // CU, 26.1 ms, and 16 copies of eight groups at one per CU lost a third: four waves per CU
-  // cannot hide the generator and table latencies).
-  const bool bf16 = sizeof(typename S::storage) == 2;
-  uint32_t copies = 0;
-  if (cap > 0) {
-    if (w.n_groups == 2 || (w.n_groups == 1 && !bf16))
-      copies = 32;
-    else if (w.n_groups == 4 && bf16)
-      copies = 16;
-  }
-  const size_t table_bytes =
-      copies ? size_t{kSpreadFloats} * sizeof(float) : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
-  const size_t static_lds = fixed ? table_bytes : 0;
-  const size_t pad = occupancy_lds(cap, static_lds);
-  const size_t tables = fixed ? 0 : table_bytes;
-  const size_t lds = tables > pad ? tables : pad;  // dynamic tables (up to 128 KiB) or the pad
-  auto go = [&](auto kernel) {
+  const uint32_t copies = sh.copies;
+  // One kernel: NG groups fixed at compile time (0: a runtime count, tables in dynamic LDS), C
+  // copies of each table, launched with the dimensions it was built for.
+  auto go = [&](auto kernel, auto groups, auto copies_c, auto dims) {
+    constexpr int NG = decltype(groups)::value, C = decltype(copies_c)::value;
+    constexpr int B = decltype(dims)::block, W = decltype(dims)::wps;
+    const size_t table_bytes = NG > 0 ? size_t{table_floats<NG, C>()} * sizeof(float)
+                                      : static_cast<size_t>(w.n_groups) * 256 * sizeof(float);
+    const size_t static_lds = NG > 0 ? table_bytes : 0;
+    const size_t pad = occupancy_lds(cap, static_lds);
+    const size_t tables = NG > 0 ? 0 : table_bytes;
+    const size_t lds = tables > pad ? tables : pad;  // dynamic tables (up to 128 KiB) or the pad
     allow_lds(kernel, lds, static_lds);
-    kernel<<<grid, block, lds, st>>>(ps, gen, w.k_base, w.K, w.n_groups, w.cf, w.lr, w.r);
+    kernel<<<grid_of(B, W), dim3(B), lds, st>>>(ps, gen, w.k_base, w.K, w.n_groups, w.cf, w.lr, w.r);
   };
+  using std::integral_constant;
+  using D256 = Dims<kBlock, 1>;
+  constexpr bool bf16 = sizeof(typename S::storage) == 2;
+  // The tables and launch dimensions shape_for picks for each group count: streaming bf16
+  // updates of two, four and eight groups take their own (two waves per stream; 512- and
+  // 1024-thread workgroups); everything else 256 threads.
   auto dispatch = [&](auto restore) {
     constexpr bool R = decltype(restore)::value;
+    using G1 = integral_constant<int, 1>;
+    using G2 = integral_constant<int, 2>;
+    using G4 = integral_constant<int, 4>;
+    using G8 = integral_constant<int, 8>;
+    using C0 = integral_constant<int, 0>;
+    using C16 = integral_constant<int, 16>;
+    using C32 = integral_constant<int, 32>;
     switch (w.n_groups) {
-      case 1: copies ? go(update_kernel<S, 1, R, N, 32>) : go(update_kernel<S, 1, R, N, 0>); break;
-      case 2: copies ? go(update_kernel<S, 2, R, N, 32>) : go(update_kernel<S, 2, R, N, 0>); break;
-      case 4: copies ? go(update_kernel<S, 4, R, N, 16>) : go(update_kernel<S, 4, R, N, 0>); break;
-      case 8: go(update_kernel<S, 8, R, N, 0>); break;
-      default: go(update_kernel<S, 0, R, N, 0>); break;
+      case 1:
+        if (copies)
+          go(update_kernel<S, 1, R, N, 32, kBlock, 1>, G1{}, C32{}, D256{});
+        else
+          go(update_kernel<S, 1, R, N, 0, kBlock, 1>, G1{}, C0{}, D256{});
+        break;
+      case 2:
+        if (!copies)
+          go(update_kernel<S, 2, R, N, 0, kBlock, 1>, G2{}, C0{}, D256{});
+        else if constexpr (!bf16)
+          go(update_kernel<S, 2, R, N, 32, kBlock, 1>, G2{}, C32{}, D256{});
+        else if constexpr (R)
+          go(update_kernel<S, 2, R, N, 32, 256, 2>, G2{}, C32{}, Dims<256, 2>{});
+        else
+          go(update_kernel<S, 2, R, N, 32, 512, 2>, G2{}, C32{}, Dims<512, 2>{});
+        break;
+      case 4:
+        if (!copies || !bf16)
+          go(update_kernel<S, 4, R, N, 0, kBlock, 1>, G4{}, C0{}, D256{});
+        else if constexpr (R)
+          go(update_kernel<S, 4, R, N, 16, 512, 1>, G4{}, C16{}, Dims<512, 1>{});
+        else
+          go(update_kernel<S, 4, R, N, 32, 1024, 1>, G4{}, C32{}, Dims<1024, 1>{});
+        break;
+      case 8:
+        if (!copies || !bf16)
+          go(update_kernel<S, 8, R, N, 0, kBlock, 1>, G8{}, C0{}, D256{});
+        else if constexpr (R)
+          go(update_kernel<S, 8, R, N, 16, 512, 1>, G8{}, C16{}, Dims<512, 1>{});
+        else
+          go(update_kernel<S, 8, R, N, 16, 1024, 1>, G8{}, C16{}, Dims<1024, 1>{});
+        break;
+      default:
+        go(update_kernel<S, 0, R, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
+        break;
     }
   };
   if (w.restore)
@@ -987,48 +911,19 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
     dispatch(std::false_type{});
 }
 
-int check_sweep(const Sweep& w) {
-  if (!std::isfinite(w.a.eps) || (w.two && !std::isfinite(w.b.eps))) return ZO_ERR_NONFINITE;
-  if (w.update && (!std::isfinite(w.lr) || (w.restore && !std::isfinite(w.r.eps)))) return ZO_ERR_NONFINITE;
-  return ZO_OK;
-}
-
-int make_update_sweep(Sweep& w, uint32_t k_base, uint32_t K, const float* c, float lr, const Probe* r) {
-  if (K > ZO_K_MAX) return ZO_ERR_ARG;
-  if (static_cast<uint64_t>(k_base) + K > (1ull << 32)) return ZO_ERR_ARG;
-  if (K > 0 && c == nullptr) return ZO_ERR_NULL;
-  if (!std::isfinite(lr) || (r && !std::isfinite(r->eps))) return ZO_ERR_NONFINITE;
-  for (uint32_t j = 0; j < K; ++j)
-    if (!std::isfinite(c[j])) return ZO_ERR_NONFINITE;
-  w = Sweep{};
-  if (K == 0) {  // nothing to sum: the restore alone, or nothing
-    w.update = false;
-    w.a = r ? *r : Probe{0, 0, 0.0f};
-    return ZO_OK;
-  }
-  w.update = true;
-  for (uint32_t j = 0; j < ZO_K_MAX; ++j) w.cf.c[j] = j < K ? c[j] : 0.0f;
-  w.k_base = k_base;
-  w.K = K;
-  const uint32_t g_first = k_base / 8;
-  const uint32_t g_last = static_cast<uint32_t>((static_cast<uint64_t>(k_base) + K - 1) / 8);
-  w.n_groups = g_last - g_first + 1;
-  w.lr = lr;
-  w.restore = r != nullptr && r->eps != 0.0f;  // a zero restore changes nothing (theta + 0 = theta)
-  w.r = r ? *r : Probe{0, 0, 0.0f};
-  return ZO_OK;
-}
-
 // One contiguous tensor.
 template <class S>
 int run_one(void* params, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step, const Sweep& w, void* stream) {
   const Shape sh = shape_for(n, sizeof(typename S::storage), w);
-  Plans<1> ps{};
-  ps.chunk_groups = sh.chunk_groups;
-  add_plan(ps, make_plan(params, offset, n, sizeof(typename S::storage), sh.chunk_groups));
+  const Gen gen = make_gen(seed, step);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const zo_segment seg{params, offset, n};
   (void)hipGetLastError();
-  launch_sweep<S>(ps, make_gen(seed, step), w, sh, static_cast<hipStream_t>(stream));
-  return launch_status();
+  // one launch (several only for a tensor of more than kPieceElems weights without full row groups)
+  return plan_segments<1>(&seg, 1, sizeof(typename S::storage), sh.chunk_groups, [&](const Plans<1>& ps) {
+    launch_sweep<S>(ps, gen, w, sh, st);
+    return launch_status();
+  });
 }
 
 int run_one_dt(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64_t seed, uint32_t step,
@@ -1042,29 +937,8 @@ int run_one_dt(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint64
                          : run_one<BF16>(params, offset, n, seed, step, w, stream);
 }
 
-// A list of tensors: validated as a whole (alignment, index ranges, no two segments sharing
-// memory), then swept in launches of up to kSegsPerLaunch segments.
-int check_segments(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype) {
-  if (dtype != ZO_F32 && dtype != ZO_BF16) return ZO_ERR_ARG;
-  if (n_segs == 0) return ZO_OK;
-  if (segs == nullptr) return ZO_ERR_NULL;
-  const size_t elem = dtype == ZO_F32 ? 4 : 2;
-  std::vector<std::pair<uintptr_t, uintptr_t>> spans;
-  spans.reserve(n_segs);
-  for (uint32_t i = 0; i < n_segs; ++i) {
-    const int rc = check_params(segs[i].params, dtype, segs[i].offset, segs[i].n);
-    if (rc != ZO_OK) return rc;
-    if (segs[i].n == 0) continue;
-    const uintptr_t a = reinterpret_cast<uintptr_t>(segs[i].params);
-    if (segs[i].n > (UINTPTR_MAX - a) / elem) return ZO_ERR_ARG;
-    spans.emplace_back(a, a + segs[i].n * elem);
-  }
-  std::sort(spans.begin(), spans.end());
-  for (size_t i = 1; i < spans.size(); ++i)
-    if (spans[i].first < spans[i - 1].second) return ZO_ERR_ARG;  // overlapping memory
-  return ZO_OK;
-}
-
+// A list of tensors (validated as a whole first), swept in launches of up to kSegsPerLaunch
+// segments.
 template <class S>
 int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_t step, const Sweep& w,
                  void* stream) {
@@ -1074,28 +948,11 @@ int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_
   for (uint32_t i = 0; i < n_segs; ++i) total += segs[i].n;
   const Shape sh = shape_for(total, sizeof(typename S::storage), w);
   (void)hipGetLastError();
-  Plans<kSegsPerLaunch> ps{};
-  ps.chunk_groups = sh.chunk_groups;
-  for (uint32_t i = 0; i < n_segs; ++i) {
-    if (segs[i].n == 0) continue;
-    const Plan pl = make_plan(segs[i].params, segs[i].offset, segs[i].n, sizeof(typename S::storage), sh.chunk_groups);
-    if (ps.count && ps.chunk_end[ps.count - 1] + static_cast<uint64_t>(plan_chunks(pl, sh.chunk_groups)) >= kMaxLaunchChunks) {
-      launch_sweep<S>(ps, gen, w, sh, st);  // keep a launch's chunk count 32-bit
-      if (launch_status() != ZO_OK) return ZO_ERR_HIP;
-      ps.count = 0;
-    }
-    add_plan(ps, pl);
-    if (ps.count == kSegsPerLaunch) {
-      launch_sweep<S>(ps, gen, w, sh, st);
-      if (launch_status() != ZO_OK) return ZO_ERR_HIP;
-      ps.count = 0;
-    }
-  }
-  if (ps.count) {
-    launch_sweep<S>(ps, gen, w, sh, st);
-    return launch_status();
-  }
-  return ZO_OK;
+  return plan_segments<kSegsPerLaunch>(segs, n_segs, sizeof(typename S::storage), sh.chunk_groups,
+                                       [&](const Plans<kSegsPerLaunch>& ps) {
+                                         launch_sweep<S>(ps, gen, w, sh, st);
+                                         return launch_status();
+                                       });
 }
 
 int run_segments_dt(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uint64_t seed, uint32_t step,
@@ -1106,14 +963,6 @@ int run_segments_dt(const zo_segment* segs, uint32_t n_segs, zo_dtype dtype, uin
   if (rs != ZO_OK) return rs;
   return dtype == ZO_F32 ? run_segments<F32>(segs, n_segs, seed, step, w, stream)
                          : run_segments<BF16>(segs, n_segs, seed, step, w, stream);
-}
-
-Sweep perturb_sweep(uint32_t k_a, float eps_a, const uint32_t* k_b, float eps_b) {
-  Sweep w{};
-  w.a = make_probe(k_a, eps_a);
-  w.two = k_b != nullptr;
-  w.b = k_b ? make_probe(*k_b, eps_b) : w.a;
-  return w;
 }
 
 }  // namespace
@@ -1185,11 +1034,11 @@ int zo_gen_bits(uint8_t* out_dev, uint64_t tile_begin, uint64_t n_tiles, uint64_
   if (reinterpret_cast<uintptr_t>(out_dev) % 16 != 0) return ZO_ERR_ARG;
   if (tile_begin >= (1ull << 60) || n_tiles > (1ull << 60) - tile_begin) return ZO_ERR_ARG;
   (void)hipGetLastError();
-  gen_bits_kernel<<<dim3(grid_for(n_tiles, kBlock)), dim3(kBlock), 0, static_cast<hipStream_t>(stream)>>>(
+  gen_bits_kernel<<<dim3(grid_for(n_tiles, kBlock, kBlock)), dim3(kBlock), 0, static_cast<hipStream_t>(stream)>>>(
       out_dev, tile_begin, n_tiles, group, make_gen(seed, step));
   return launch_status();
 }
 
-void zo_set_max_blocks(uint32_t max_blocks) { g_max_blocks = max_blocks; }
+void zo_set_max_blocks(uint32_t max_blocks) { set_max_blocks(max_blocks); }
 
 }  // extern "C"

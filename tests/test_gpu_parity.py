@@ -504,10 +504,11 @@ def test_segments_streaming_shape_equal_flat_bits():
     """Above the 256 MiB streaming threshold: 56 separately allocated tensors of ragged sizes
     (tiny ones among multi-million ones, none a multiple of the 32 KiB chunk, the first at a
     global offset of 777) get, in every element, the bits that the single-buffer calls give
-    the same values laid out flat: perturb, a two-probe transition, the update with restore at
-    K = 16 (streaming shape, one chunk per wave), the update and the update with restore at
-    K = 32 (16-copy tables, two workgroups per CU) and the update at K = 64 (short chunks). The
-    single-buffer calls are themselves checked against the oracle at full size."""
+    the same values laid out flat: perturb, a two-probe transition, the update and the update
+    with restore at K = 16 (two waves per stream, one chunk per stream), K = 32 (two-plane
+    32-copy tables in 1024-thread workgroups; 16-copy tables at two workgroups per CU) and
+    K = 64 (16-copy tables shared by 1024 or 512 threads). The single-buffer calls are
+    themselves checked against the oracle at full size."""
     rng = np.random.default_rng(13)
     sizes = [int(x) for x in rng.integers(1, 8_000_000, 50)] + [1, 7, 1023, 1024, 1025, 16_385]
     sizes = [sizes[i] for i in rng.permutation(len(sizes))]
@@ -537,6 +538,9 @@ def test_segments_streaming_shape_equal_flat_bits():
     zo.zo_perturb2(flat, 3, -2 * eps, 12, eps, seed, step, offset=base)
     zo.zo_perturb_segments(ts, offs, 3, -2 * eps, 12, eps, seed, step)
     same("perturb2")
+    zo.zo_update_ex(flat, c16, lr, seed, step, offset=base)
+    zo.zo_update_segments(ts, offs, c16, lr, seed, step)
+    same("update K=16")
     zo.zo_update_restore(flat, c16, lr, seed, step, 12, -eps, offset=base)
     zo.zo_update_segments(ts, offs, c16, lr, seed, step, 12, -eps)
     same("update_restore K=16")
@@ -549,6 +553,43 @@ def test_segments_streaming_shape_equal_flat_bits():
     zo.zo_update_ex(flat, c64, lr, seed, step, offset=base)
     zo.zo_update_segments(ts, offs, c64, lr, seed, step)
     same("update K=64")
+    zo.zo_update_restore(flat, c64, lr, seed, step, 63, -eps, offset=base)
+    zo.zo_update_segments(ts, offs, c64, lr, seed, step, 63, -eps)
+    same("update_restore K=64")
+
+
+@pytest.mark.parametrize("op", ["perturb", "update16", "restore16", "update32", "restore32", "update64", "restore64"])
+def test_streaming_results_independent_of_grid(op):
+    """Above the streaming threshold, where the launches use two waves per stream, one or four
+    chunks per stream and 512- or 1024-thread workgroups: capping the grid at 1, 7 or 300
+    workgroups (every stream then loops over many chunks) leaves every bit of the result as
+    the default grid gives it."""
+    n = 144_000_019
+    note(f"streaming grid independence: {op}")
+    src = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(21)
+    src.normal_(0.0, 0.02, generator=gen)
+    c = np.random.default_rng(5).standard_normal(64).astype(np.float32)
+    outs = []
+    try:
+        for blocks in (0, 1, 7, 300):
+            zo.zo_set_max_blocks(blocks)
+            t = src.clone()
+            if op == "perturb":
+                zo.zo_perturb(t, 11, 1e-3, 5, 1, offset=33)
+            else:
+                K = int(op[-2:])
+                if op.startswith("update"):
+                    zo.zo_update_ex(t, c[:K], 1e-3, 5, 1, offset=33)
+                else:
+                    zo.zo_update_restore(t, c[:K], 1e-3, 5, 1, K - 1, 1e-3, offset=33)
+            torch.cuda.synchronize()
+            outs.append(t)
+    finally:
+        zo.zo_set_max_blocks(0)
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
 
 
 def test_concurrent_streams_on_disjoint_tensors():
