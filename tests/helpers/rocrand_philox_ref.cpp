@@ -10,7 +10,14 @@ int main() {
   unsigned long long seed, tile, step, group;
   while (std::scanf("%llu %llu %llu %llu", &seed, &tile, &step, &group) == 4) {
     const unsigned long long subsequence = step | (group << 32);
-    rocrand_device::philox4x32_10_engine eng(seed, subsequence, 4ull * tile);
+    rocrand_device::philox4x32_10_engine eng(seed, subsequence, 0);
+    // advance the counter's low 64 bits by `tile` blocks (four numbers each), in pieces whose
+    // number count stays below 2^64
+    for (unsigned long long left = tile; left;) {
+      const unsigned long long piece = left < (1ull << 60) ? left : (1ull << 60);
+      eng.discard(4ull * piece);
+      left -= piece;
+    }
     uint4 r = eng.next4();
     std::printf("%u %u %u %u\n", r.x, r.y, r.z, r.w);
   }
