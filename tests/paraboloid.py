@@ -33,11 +33,24 @@ def steps_to_converge(backend, x, lr, K, eps, alpha, max_steps, tol):
 
 
 def best_steps(make_backend, lrs, K, eps, alpha, max_steps, tol):
-    """Fewest steps over a grid of step sizes (each solver gets its own tuned step size)."""
+    """Fewest steps over a grid of step sizes (each solver gets its own tuned step size).
+    The largest step size runs first and every later run stops once it cannot beat the best
+    count so far, which leaves the minimum unchanged. None if every run diverges."""
     best = None
-    for lr in lrs:
+    for lr in sorted(lrs, reverse=True):
         backend, x0 = make_backend()
-        n = steps_to_converge(backend, x0, lr, K, eps, alpha, max_steps, tol)
+        n = steps_to_converge(backend, x0, lr, K, eps, alpha, max_steps if best is None else best, tol)
         if n is not None and (best is None or n < best):
             best = n
     return best
+
+
+def trend(job, kappas, alphas, seeds, procs):
+    """{(kappa, alpha, seed): best steps} for every combination, job((kappa, alpha, seed))
+    computing one entry, in `procs` forked worker processes."""
+    import multiprocessing
+    keys = [(k, a, s) for k in kappas for a in alphas for s in seeds]
+    # the slowest combinations (large kappa, plain 1SPSA) first, so that the pool stays busy
+    keys.sort(key=lambda t: (-t[0], t[1]))
+    with multiprocessing.get_context("fork").Pool(procs) as pool:
+        return dict(zip(keys, pool.map(job, keys, chunksize=1)))
