@@ -148,9 +148,12 @@ int zo_perturb2(void* params, zo_dtype dtype, uint64_t offset, uint64_t n, uint6
  * zo_update_restore -- theta[i] <- theta[i] + eps_restore z_{k_restore}[offset+i]
  *                                  - lr * sum_j c[j] z_{k_base+j}[offset+i], one sweep:
  * the last probe's restore merged with the fused update (Algorithm 1's final +eps and its
- * rank-0 update loop; section 4.2, Eq. 6). Arithmetic per element in fp32:
- * t = fl(theta + eps_restore z), then t - s with s as in zo_update, then one rounding to
- * bf16 for bf16 weights. eps_restore = 0 gives zo_update_ex's result bit for bit.
+ * rank-0 update loop; section 4.2, Eq. 6). Arithmetic per element in fp32, s as in
+ * zo_update: when k_restore lies in one of the update's probe groups (8 j .. 8 j + 7 for a
+ * group j that holds one of the K probes; Algorithm 1 restores probe k_base + K - 1), that
+ * group's term fl(lr * t_g) becomes fl(fl(lr * t_g) - eps_restore z) and the result is
+ * theta - s; otherwise t = fl(theta + eps_restore z), then t - s. Then one rounding to bf16
+ * for bf16 weights. eps_restore = 0 gives zo_update_ex's result bit for bit.
  * Errors: as zo_update_ex (ZO_ERR_NONFINITE also for a non-finite eps_restore). With K = 0
  * it applies the restore alone.
  */

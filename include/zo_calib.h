@@ -15,16 +15,24 @@ extern "C" {
 #endif
 
 /* XOR every 16-byte vector of p[0 .. bytes) in place with `key` replicated four times:
- * one read and one write of every byte, in the streaming shape of the perturb sweep (each
- * wave walks up to 32 KiB in 2 KiB steps with the next two steps' loads in flight,
- * non-temporal loads and stores, one workgroup of 256 threads per CU at a time, grid-stride
- * over up to 65,536 workgroups) and no other work. Two calls with the same key restore the
- * buffer bit for bit.
- *   p      caller-owned device memory, 16-byte aligned; bytes a multiple of 16.
+ * one read and one write of every byte, by the sweeps' own streaming loop and launch plan
+ * (the buffer taken as bf16 weights: each wave walks up to 32 KiB in 2 KiB row groups with
+ * the next two groups' loads in flight, non-temporal loads and stores, one workgroup of 256
+ * threads per CU at a time, grid-stride over up to 65,536 workgroups) and no other work. Two
+ * calls with the same key restore the buffer bit for bit.
+ *   p      caller-owned device memory, 16-byte aligned; bytes a multiple of 16, below 2^41.
  *   stream hipStream_t (NULL = default stream); the call is asynchronous on it.
  * Returns 0; -1 for p == NULL with bytes > 0; -2 for misalignment or a size that is not a
- * multiple of 16 (nothing launched); -4 when the launch fails. bytes == 0 is a no-op. */
+ * multiple of 16 or too large (nothing launched); -4 when the launch fails. bytes == 0 is a
+ * no-op. */
 int zo_calib_rmw(void* p, uint64_t bytes, uint32_t key, void* stream);
+
+/* zo_calib_rmw in another launch shape, so that the ceiling can be taken as the fastest of
+ * several: shape bit 0 = one 32 KiB chunk per wave (a grid sized to the buffer instead of
+ * grid-stride), bit 1 = paced (each step of three groups first waits until at most four memory
+ * operations of the wave are outstanding). shape 0 is zo_calib_rmw. Returns as zo_calib_rmw,
+ * and -2 also for shape bits above bit 1 (nothing launched). */
+int zo_calib_rmw_shape(void* p, uint64_t bytes, uint32_t key, uint32_t shape, void* stream);
 
 #ifdef __cplusplus
 }

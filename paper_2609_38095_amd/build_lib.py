@@ -1,5 +1,6 @@
 """Compile libzo.so for gfx950 in-tree (hipcc for the HIP sweep, the host compiler for the rest),
-and libzo_calib.so, the read-modify-write ceiling probe the benchmark measures beside it."""
+and libzo_calib.so, the read-modify-write ceiling probe the benchmark measures beside it (the
+sweeps' streaming loop with the probe work replaced by an XOR)."""
 
 import os
 import shutil
@@ -51,8 +52,13 @@ def build(verbose=False):
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB)
+    # the ceiling kernel runs the sweeps' streaming loop (csrc/zo_stream.h) under their launch
+    # plan (the host planner's object, linked in)
+    calib_obj = os.path.join(BUILD, "rmw_ceiling.hip.o")
+    _run([HIPCC, *DEVICE_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", CALIB_SRC, "-o", calib_obj], verbose)
     tmp = CALIB_LIB + ".tmp"
-    _run([HIPCC, *DEVICE_FLAGS, "-I", INCLUDE, "-shared", "-o", tmp, CALIB_SRC], verbose)
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, calib_obj,
+          os.path.join(BUILD, "zo_plan.cpp.o")], verbose)
     os.replace(tmp, CALIB_LIB)
     return LIB
 

@@ -1,124 +1,77 @@
 // Measurement aid, not part of the method: the plain in-place read-modify-write ceiling of a
-// buffer. Every 16-byte vector is XORed with a 32-bit key replicated four times, in the
-// streaming shape of the bf16 perturb sweep and with no other work: each wave walks a chunk
-// of up to 32 KiB in steps of 2 KiB (two rows of 64 lanes x 16 bytes, non-temporal loads and
-// stores) with the loads of the next two steps in flight, grid-stride over chunks with
-// 65,536 workgroups of 256 threads, one workgroup per CU at a time (dynamic LDS). Two calls
-// with the same key restore the buffer exactly.
+// buffer. Every 16-byte vector is XORed with a 32-bit key replicated four times, with no other
+// work, by the sweeps' own streaming loop (zo_stream.h) over the buffer taken as bf16 weights:
+// row groups of two rows of 64 lanes x 16 bytes, non-temporal loads and stores, chunks of up
+// to 32 KiB per wave with the loads of the next two groups in flight, one workgroup of 256
+// threads per CU at a time (dynamic LDS), and the sweeps' launch plan (zo_plan.cpp). Shapes:
+// grid-stride over up to 65,536 workgroups or one chunk per wave, unpaced or paced at four
+// outstanding memory operations, as the sweeps are launched. Two calls with the same key
+// restore the buffer exactly.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
+#include "zo_plan.h"
+#include "zo_stream.h"
+
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-constexpr uint32_t kBlock = 256;
-constexpr uint64_t kStepVecs = 128;      // 2 KiB per wave step
-constexpr uint64_t kChunkSteps = 16;     // 32 KiB per wave chunk
-constexpr uint32_t kGrid = 65536;
-constexpr size_t kOnePerCuLds = 96 * 1024;
+using namespace zo;
 
-__device__ __forceinline__ void load_step(u32x4 (&d)[2], const u32x4* q) {
-  d[0] = __builtin_nontemporal_load(q);
-  d[1] = __builtin_nontemporal_load(q + 64);
-}
-__device__ __forceinline__ void store_step(u32x4* q, const u32x4 (&d)[2], u32x4 k) {
-  __builtin_nontemporal_store(d[0] ^ k, q);
-  __builtin_nontemporal_store(d[1] ^ k, q + 64);
-}
-
-__global__ __launch_bounds__(kBlock) void xor_sweep(u32x4* p, uint64_t n_vecs, uint32_t key) {
-  extern __shared__ uint32_t occupancy_pad[];
-  if (key == 0 && n_vecs == 0) occupancy_pad[threadIdx.x] = 0;  // never taken (n_vecs > 0)
+template <int PACE>
+__global__ __launch_bounds__(kBlock) void xor_sweep(Plans<1> ps, uint32_t key) {
+  extern __shared__ uint32_t occupancy_pad[];  // dynamic LDS only limits workgroups per CU
+  if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count is 1)
   const u32x4 k = {key, key, key, key};
-  const uint32_t lane = threadIdx.x & 63u;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t n_waves = gridDim.x * (kBlock / 64);
-  // 32-bit step and chunk indices (the host keeps a call below 2^31 chunks): the loop
-  // control stays on the scalar unit
-  const uint32_t n_steps = static_cast<uint32_t>(n_vecs / kStepVecs);
-  const uint32_t n_chunks = (n_steps + kChunkSteps - 1) / kChunkSteps;
-  for (uint32_t c = blockIdx.x * (kBlock / 64) + wave; c < n_chunks; c += n_waves) {
-    const uint32_t s0 = c * kChunkSteps, s1 = s0 + kChunkSteps < n_steps ? s0 + kChunkSteps : n_steps;
-    u32x4* q = p + static_cast<uint64_t>(s0) * kStepVecs + lane;
-    // rotating register sets with the loads of the next two steps in flight, and one full
-    // step run before the loop so that the loop is entered with the same memory operations
-    // outstanding as on its back edge (as the perturb sweep)
-    u32x4 x[2], y[2], z[2];
-    auto prefetch2 = [&](u32x4 (&d)[2]) {
-      load_step(d, q + 2 * kStepVecs);
-      __builtin_amdgcn_sched_barrier(0);
-    };
-    auto work = [&](const u32x4 (&d)[2]) {
-      store_step(q, d, k);
-      q += kStepVecs;
-    };
-    auto step3 = [&]() {
-      prefetch2(z);
-      work(x);
-      prefetch2(x);
-      work(y);
-      prefetch2(y);
-      work(z);
-    };
-    auto last = [&](uint32_t left) {  // 2 to 4 steps left, x and y requested
-      if (left >= 3) {
-        prefetch2(z);
-        work(x);
-        if (left == 4) {
-          prefetch2(x);
-          work(y);
-          work(z);
-          work(x);
-        } else {
-          work(y);
-          work(z);
+  constexpr int R = GroupShape<BF16>::kRows;
+  for_each_group<BF16, 2, 1, PACE, kBlock, 1>(
+      ps,
+      [&](uint64_t, u32x4 (&d)[R], uint32_t) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+          // the empty asm makes the XOR opaque: with a body this light the compiler otherwise
+          // keeps the loop's rotating register sets in scratch memory
+          u32x4 t = d[u] ^ k;
+          asm volatile("" : "+v"(t));
+          d[u] = t;
         }
-      } else {
-        work(x);
-        work(y);
-      }
-    };
-    load_step(x, q);
-    uint32_t s = s0;
-    if (s + 4 < s1) {
-      load_step(y, q + kStepVecs);
-      step3();
-      s += 3;
-      for (; s + 4 < s1; s += 3) step3();
-      last(s1 - s);
-    } else if (s + 1 < s1) {
-      load_step(y, q + kStepVecs);
-      last(s1 - s);
-    } else {
-      work(x);
-    }
-  }
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-  for (uint64_t v = static_cast<uint64_t>(n_steps) * kStepVecs + static_cast<uint64_t>(blockIdx.x) * kBlock +
-                    threadIdx.x;
-       v < n_vecs; v += stride)
-    p[v] = p[v] ^ k;
+      },
+      []() {});
+  // head and tail elements: element g of the buffer is XORed with the key's low 16 bits
+  // (g even) or high 16 bits (g odd), as the 16-byte XOR does
+  for_each_edge<1, kBlock>(ps, [&](const Plan& pl, uint64_t t) {
+    uint16_t* p = reinterpret_cast<uint16_t*>(pl.base);
+    for (uint64_t g = t * kTile; g < (t + 1) * kTile; ++g)
+      if (g >= pl.lo && g < pl.hi) p[g - pl.lo] ^= static_cast<uint16_t>(g & 1 ? key >> 16 : key);
+  });
 }
 
 }  // namespace
 
-// 0 on success; -1 for a null pointer with bytes > 0; -2 when p is not 16-byte aligned,
-// bytes is not a multiple of 16 or reaches 2^46; -4 when the launch fails. Asynchronous on
-// `stream`.
-extern "C" int zo_calib_rmw(void* p, uint64_t bytes, uint32_t key, void* stream) {
+// shape: bit 0 one chunk per wave, bit 1 paced. 0 on success; -1 for a null pointer with
+// bytes > 0; -2 when p is not 16-byte aligned, bytes is not a multiple of 16 or reaches 2^41,
+// or shape has other bits; -4 when the launch fails. Asynchronous on `stream`.
+extern "C" int zo_calib_rmw_shape(void* p, uint64_t bytes, uint32_t key, uint32_t shape, void* stream) {
   if (bytes == 0) return 0;
   if (p == nullptr) return -1;
   if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0 || (bytes & 15u) != 0) return -2;
-  if (bytes >= (1ull << 46)) return -2;  // 2^31 chunks of 32 KiB
-  const uint64_t n_vecs = bytes / 16;
-  const uint64_t chunks = (n_vecs / kStepVecs + kChunkSteps - 1) / kChunkSteps;
-  uint64_t blocks = (chunks + 3) / 4;
-  if (blocks < 1) blocks = 1;
-  if (blocks > kGrid) blocks = kGrid;
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(xor_sweep), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            static_cast<int>(kOnePerCuLds));
-  hipLaunchKernelGGL(xor_sweep, dim3(static_cast<uint32_t>(blocks)), dim3(kBlock), kOnePerCuLds,
-                     static_cast<hipStream_t>(stream), static_cast<u32x4*>(p), n_vecs, key);
+  if (bytes / 2 >= ZO_N_MAX) return -2;
+  if (shape & ~3u) return -2;
+  const bool one_chunk_per_wave = shape & 1u, paced = shape & 2u;
+  const Shape sh{static_cast<uint32_t>(kMaxChunkBytes / (kGroupElems * 2)), 1, one_chunk_per_wave ? 1u : 0u};
+  Plans<1> ps{};
+  ps.chunk_groups = sh.chunk_groups;
+  add_plan(ps, make_plan(p, 0, bytes / 2, 2, sh.chunk_groups));
+  const size_t pad = occupancy_lds(sh.blocks_per_cu, 0);
+  auto kernel = paced ? xor_sweep<4> : xor_sweep<0>;
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(pad));
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(kernel, dim3(plans_grid(ps, sh)), dim3(kBlock), pad, static_cast<hipStream_t>(stream), ps,
+                     key);
   return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+extern "C" int zo_calib_rmw(void* p, uint64_t bytes, uint32_t key, void* stream) {
+  return zo_calib_rmw_shape(p, bytes, key, 0, stream);
 }

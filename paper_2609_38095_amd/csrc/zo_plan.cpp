@@ -117,25 +117,24 @@ Gen make_gen(uint64_t seed, uint32_t step) {
 //     6.53 TB/s);
 //   update, two bf16 groups: 512 threads, two waves per stream, one chunk per stream, 32-copy
 //     tables (OPT-13B K = 16: +0.5 to 1.8%, +2% on a GPU already busy with perturbs);
-//     with restore, 256 threads, two waves per stream, two workgroups per CU (+0.7 to 4%);
 //   update, three bf16 groups: three workgroups per CU, one group ahead;
 //   update, four bf16 groups: 1024 threads, 32-copy tables in two planes (OPT-30B K = 32:
-//     21.9 -> 21.6 ms); with restore, 512 threads, 16-copy tables, two workgroups per CU
-//     (23.5 -> 22.9 ms);
+//     21.9 -> 21.6 ms);
 //   update, eight bf16 groups (K = 57-64): 1024 threads sharing 16-copy tables in two planes
 //     (4 LDS cycles per 64-lane read instead of 6.3), four chunks per stream (OPT-1.3B K = 64:
-//     1.80 -> 1.57 ms; Qwen3-8B K = 60: 10.9 -> 9.9 ms); with restore, 512 threads (1024 would
-//     spill registers: 2.26 -> 1.82 ms and 11.85 -> 11.27 ms);
+//     1.80 -> 1.57 ms; Qwen3-8B K = 60: 10.9 -> 9.9 ms);
 //   fp32 updates: one workgroup per CU up to three groups, two at four, three at five or six.
-// Other updates (five to seven bf16 groups, more than eight, or more than six in fp32) are
-// bound by the generator or the LDS table lookups and keep 4 KiB chunks at full occupancy, as
-// do sweeps smaller than the 256 MiB Infinity Cache. Grids: up to kDefaultMaxBlocks
-// workgroups, grid-stride beyond (in-order dispatch of many short-lived workgroups keeps the
-// streams compact; a persistent grid of one workgroup per CU measured 5.6 TB/s), except where
-// a number of chunks per stream is given: the one-probe bf16 perturb, the two-probe fp32
-// perturb and the bf16 updates of one or two groups run one chunk per stream (OPT-13B: the
-// perturb 6.48 -> 6.67 TB/s, OPT-30B 6.20 -> 6.60; 3 G fp32 weights: the two-probe perturb
-// 6.30 -> 6.48 across two probe groups).
+// An update with a restore probe inside its groups (Algorithm 1's schedule) is the plain
+// update with that group's table changed, and takes the update's shape. Other updates (five to
+// seven bf16 groups, more than eight, or more than six in fp32, and a restore probe outside
+// the update's groups) are bound by the generator or the LDS table lookups and keep 4 KiB
+// chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity Cache. Grids: up to
+// kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of many short-lived
+// workgroups keeps the streams compact; a persistent grid of one workgroup per CU measured
+// 5.6 TB/s), except where a number of chunks per stream is given: the one-probe bf16 perturb,
+// the two-probe fp32 perturb and the bf16 updates of one or two groups run one chunk per stream
+// (OPT-13B: the perturb 6.48 -> 6.67 TB/s, OPT-30B 6.20 -> 6.60; 3 G fp32 weights: the
+// two-probe perturb 6.30 -> 6.48 across two probe groups).
 Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   const uint64_t group_bytes = kGroupElems * elem;
   const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0, 0};
@@ -145,6 +144,7 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
     const bool one_probe_bf16 = !w.two && elem == 2, two_probes_fp32 = w.two && elem == 4;
     return Shape{chunk, 1, one_probe_bf16 || two_probes_fp32 ? 1u : 0u};
   }
+  if (w.restore && !w.fold) return short_chunks;
   const uint32_t g = w.n_groups;
   Shape sh{chunk, 1, 0};
   if (elem == 4) {
@@ -161,33 +161,19 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
       sh.copies = 32;
       sh.wps = 2;
       sh.chunks_per_wave = 1;
-      if (w.restore) {
-        sh.blocks_per_cu = 2;
-      } else {
-        sh.block = 512;
-      }
+      sh.block = 512;
       return sh;
     case 3:
       sh.blocks_per_cu = 3;
       return sh;
     case 4:
-      if (w.restore) {
-        sh.block = 512;
-        sh.copies = 16;
-        sh.blocks_per_cu = 2;
-      } else {
-        sh.block = 1024;
-        sh.copies = 32;
-      }
+      sh.block = 1024;
+      sh.copies = 32;
       return sh;
     case 8:
       sh.copies = 16;
-      if (w.restore) {
-        sh.block = 512;
-      } else {
-        sh.block = 1024;
-        sh.chunks_per_wave = 4;
-      }
+      sh.block = 1024;
+      sh.chunks_per_wave = 4;
       return sh;
     default:
       return short_chunks;
@@ -231,6 +217,7 @@ int make_update_sweep(Sweep& w, uint32_t k_base, uint32_t K, const float* c, flo
   w.lr = lr;
   w.restore = r != nullptr && r->eps != 0.0f;  // a zero restore changes nothing (theta + 0 = theta)
   w.r = r ? *r : Probe{0, 0, 0.0f};
+  w.fold = w.restore && r->group - g_first < w.n_groups;  // wraps for a group below g_first
   return ZO_OK;
 }
 

@@ -73,6 +73,8 @@ struct Coefs {
 };
 
 // What one sweep applies: one or two probes, or the update (with an optional restore probe).
+// fold: the restore probe lies in one of the update's probe groups, so its +-eps is merged
+// into that group's table and the sweep runs the plain update's per-element code.
 struct Sweep {
   bool update;
   Probe a, b;
@@ -82,6 +84,7 @@ struct Sweep {
   float lr;
   Probe r;
   bool restore;
+  bool fold;
 };
 
 // The launch shape of a sweep.

@@ -7,21 +7,12 @@
 // block per 16-element tile and probe group of 8, 8 probe signs per byte (section 4.3).
 // Nothing but theta touches HBM.
 //
-// Memory layout of a sweep. theta is walked in row groups of 1024 elements: 2 (bf16) or 4
-// (fp32) rows of 64 contiguous 16-byte vectors, one vector per lane and row, so each load and
-// store instruction of a wave covers 1 KiB of contiguous memory (non-temporal: nothing is
-// reused). A tile spans 2 vectors (bf16) or 4 (fp32); the lanes holding one tile are m and
-// m + 32 (bf16) or m, m + 16, m + 32, m + 48 (fp32), so that the gfx950 half-wave swaps
-// v_permlane32_swap / v_permlane16_swap exchange the generator words: each lane runs one
-// Philox block per row group and probe group, then bf16 lane pairs swap two words (two
-// instructions) and fp32 lane groups transpose a 4x4 word matrix (four instructions). A wave
-// streams a chunk of consecutive row groups (up to 32 KiB) with the loads of the next one or
-// two groups in flight while it works on the current one, and large sweeps cap the
-// workgroups per CU (few long read-write streams keep HBM busiest). The loops are written so
-// that the compiler's memory waits are exact, and the lightest perturbs are paced explicitly.
-// Head and tail elements that do not fill a row group (and everything, when the storage is
-// not 16-byte aligned relative to the global index) take an element-wise path, one tile per
-// lane.
+// Each lane runs one Philox block per row group (1024 elements, zo_stream.h) and probe group:
+// bf16 lane pairs then swap two generator words (v_permlane32_swap, two instructions) and
+// fp32 lane groups transpose a 4x4 word matrix (v_permlane32_swap / v_permlane16_swap, four
+// instructions), so that every lane holds the probe bytes of its own vectors. Large sweeps cap
+// the workgroups per CU (few long read-write streams keep HBM busiest), and the lightest
+// perturbs are paced.
 //
 // zo_perturb_segments / zo_update_segments sweep a list of separate tensors: the host validates
 // the list, builds one plan per tensor and launches batches of up to 64 plans (kernel
@@ -30,10 +21,11 @@
 //
 // The update keeps, per probe group, a 256-entry table in LDS: entry b is lr times the signed
 // sum of the group's 8 coefficients selected by the bits of b (pairwise), so applying 8 probes
-// to an element costs a byte extract and an LDS read, and the step is one subtraction; with one or two groups in a streaming launch
-// the tables are spread over 32 copies so that each lane reads its own LDS bank. Groups
-// accumulate in fp32, sequentially within runs of 8 groups and with Neumaier compensation
-// across runs.
+// to an element costs a byte extract and an LDS read, and the step is one subtraction. The
+// restore of a probe in one of the update's groups is merged into that group's entries. In
+// streaming launches the tables are spread over 16 or 32 copies so that lanes read different
+// LDS banks. Groups accumulate in fp32, sequentially within runs of 8 groups and with Neumaier
+// compensation across runs.
 //
 // Built with -ffp-contract=off: every product and sum is rounded as written.
 
@@ -45,14 +37,12 @@
 
 #include "zo.h"
 #include "zo_plan.h"
+#include "zo_stream.h"
 
 namespace {
 
 using namespace zo;
 
-// s_waitcnt immediate for vmcnt(n), n < 16, that leaves expcnt and lgkmcnt unconstrained
-// (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
-constexpr int wait_vmcnt(int n) { return 0x0F70 | n; }
 constexpr int kRounds = 10;
 
 // ---------------------------------------------------------------------------------------
@@ -103,85 +93,6 @@ __device__ __forceinline__ float table_at(const float* tab, uint32_t w, int e) {
   return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(tab) + off);
 }
 
-// ---------------------------------------------------------------------------------------
-// Storage formats.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ u32x4 ld_stream(const void* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-}
-__device__ __forceinline__ void st_stream(void* p, u32x4 v) {
-  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
-}
-
-// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const f32x2 v = {lo, hi};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
-
-// A storage type moves 16-byte vectors of kVecElems elements, widened to fp32. kLanesPerTile
-// adjacent lanes hold one 16-element tile; each of them needs kWords of the tile's 4
-// generator words (word w carries the probe bytes of tile elements 4w .. 4w+3).
-struct F32 {
-  typedef float storage;
-  static constexpr int kVecElems = 4, kLanesPerTile = 4, kWords = 1;
-  __device__ static __forceinline__ void unpack(u32x4 d, float (&v)[kVecElems]) {
-    v[0] = __uint_as_float(d.x);
-    v[1] = __uint_as_float(d.y);
-    v[2] = __uint_as_float(d.z);
-    v[3] = __uint_as_float(d.w);
-  }
-  __device__ static __forceinline__ u32x4 pack(const float (&v)[kVecElems]) {
-    return u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
-  }
-  __device__ static __forceinline__ float load1(const storage* p) { return *p; }
-  __device__ static __forceinline__ void store1(storage* p, float v) { *p = v; }
-};
-
-struct BF16 {
-  typedef uint16_t storage;
-  static constexpr int kVecElems = 8, kLanesPerTile = 2, kWords = 2;
-  __device__ static __forceinline__ void unpack(u32x4 d, float (&v)[kVecElems]) {
-    const uint32_t w[4] = {d.x, d.y, d.z, d.w};
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      v[2 * m] = __uint_as_float(w[m] << 16);
-      v[2 * m + 1] = __uint_as_float(w[m] & 0xFFFF0000u);
-    }
-  }
-  __device__ static __forceinline__ u32x4 pack(const float (&v)[kVecElems]) {
-    return u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
-                 pack_bf16x2(v[6], v[7])};
-  }
-  __device__ static __forceinline__ float load1(const storage* p) {
-    return __uint_as_float(static_cast<uint32_t>(*p) << 16);
-  }
-  __device__ static __forceinline__ void store1(storage* p, float v) {
-    *p = static_cast<uint16_t>(pack_bf16x2(v, 0.0f) & 0xFFFFu);
-  }
-};
-
-// A row group: kRows rows of 64 contiguous 16-byte vectors (one vector per lane and row),
-// 1024 elements, i.e. one Philox block per lane and probe group.
-template <class S>
-struct GroupShape {
-  static constexpr int kRows = S::kLanesPerTile;                // bf16 2, fp32 4
-  static constexpr uint64_t kVecs = 64ull * kRows;
-  static constexpr uint64_t kElems = kVecs * S::kVecElems;
-  static constexpr uint64_t kBytes = kVecs * 16;                // bf16 2 KiB, fp32 4 KiB
-  static_assert(kElems == kGroupElems, "a row group holds 1024 elements");
-};
-
-// Group vector held by a lane (for every row u, lane l holds group vector 64u + vec_of_lane(l)):
-// the lanes of one tile sit 32 (bf16) or 16 (fp32) lanes apart.
-template <class S>
-__device__ __forceinline__ uint32_t vec_of_lane(uint32_t lane) {
-  return S::kLanesPerTile == 2 ? 2 * (lane & 31u) + (lane >> 5) : 4 * (lane & 15u) + (lane >> 4);
-}
-
 // For a row group starting at global vector vbase (a multiple of GroupShape::kVecs) and probe
 // group g: W[u][w] = the generator words this lane's vector in row u needs.
 // bf16: lanes m and m + 32 hold the two halves of tile T(u) = vbase/2 + 32u + m; lane m + 32q
@@ -230,260 +141,6 @@ __device__ __forceinline__ void group_words(const Gen& gen, uint64_t vbase, uint
 template <class S>
 __device__ __forceinline__ uint32_t elem_byte(const uint32_t (&w)[S::kWords], int e) {
   return word_byte(w[e >> 2], e & 3);
-}
-
-// Element-wise path: elements of tile t inside [lo, hi), one lane; params holds global
-// element lo.
-template <class S, class F>
-__device__ __forceinline__ void tile_elementwise(typename S::storage* params, uint64_t lo, uint64_t hi, uint64_t t,
-                                                 F f) {
-  const uint64_t g0 = t * kTile;
-#pragma unroll
-  for (int j = 0; j < (int)kTile; ++j) {
-    const uint64_t g = g0 + j;
-    if (g >= lo && g < hi) {
-      typename S::storage* p = params + (g - lo);
-      S::store1(p, f(j, S::load1(p)));
-    }
-  }
-}
-
-// The first segment s in [from, count) with x < ends[s], where ends is nondecreasing and
-// x < ends[count - 1]: a binary search, so that finding a chunk's segment costs at most
-// log2(N) + 1 argument loads wherever the chunk lies.
-template <int N>
-__device__ __forceinline__ uint32_t segment_of(const uint32_t (&ends)[N], uint32_t from, uint32_t count, uint32_t x) {
-  uint32_t lo = from, hi = count - 1;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (x < ends[mid])
-      hi = mid;
-    else
-      lo = mid + 1;
-  }
-  return lo;
-}
-
-template <class S>
-__device__ __forceinline__ void load_group(u32x4 (&d)[GroupShape<S>::kRows], const char* base, uint32_t lane) {
-  const uint32_t v = vec_of_lane<S>(lane);
-#pragma unroll
-  for (int u = 0; u < GroupShape<S>::kRows; ++u) d[u] = ld_stream(base + 16 * (64 * u + v));
-}
-
-template <class S>
-__device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupShape<S>::kRows], uint32_t lane) {
-  const uint32_t v = vec_of_lane<S>(lane);
-#pragma unroll
-  for (int u = 0; u < GroupShape<S>::kRows; ++u) st_stream(base + 16 * (64 * u + v), d[u]);
-}
-
-// Calls body(vbase, d, lane) for every full row group of the launch, where vbase is the
-// group's global vector index and d its data, and stores what the body leaves in d. Each
-// chunk is one stream walked in address order by WPS waves of a workgroup of BLOCK threads:
-// wave w of the stream takes the chunk's groups w, w + WPS, w + 2 WPS, ..., with the loads of
-// its next AHEAD groups in flight while the body works on the current one (a stream of up to
-// 32 KiB, reads and writes interleaved). More waves per stream give the generator and table
-// work more waves to hide behind without adding streams. A wave's chunk indices increase,
-// so its segment cursor only moves forward. PACE > 0 (two ahead only): each step of three
-// groups first waits until at most PACE memory operations of the wave are outstanding: with
-// 2, only the step's own prefetch; with 4, also the previous step's last stores. The
-// lightest sweeps stream HBM faster paced (OPT-13B bf16 perturb: 6.40 TB/s with every
-// request the loop allows in flight, 6.67 paced at 2, 6.76 at 4; pacing at 6 or 8 measured
-// lower), heavier ones need the overlap.
-// prologue() runs once per wave, after the loads of the wave's first group are issued (at
-// once for a wave without groups), so that work such as building the update's LDS tables
-// overlaps their latency; it may hold a workgroup barrier, which every wave reaches once.
-template <class S, int AHEAD, int N, int PACE = 0, int BLOCK = 256, int WPS = 1, class Body, class Prologue>
-__device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Prologue prologue) {
-  static_assert(PACE == 0 || (AHEAD >= 2 && PACE >= 2 && PACE < 16), "pacing applies to the two- and three-ahead loops");
-  static_assert(AHEAD >= 1 && AHEAD <= 3, "one to three groups in flight");
-  static_assert(BLOCK % 64 == 0 && (WPS == 1 || WPS == 2 || WPS == 4) && (BLOCK / 64) % WPS == 0,
-                "whole streams per workgroup");
-  using G = GroupShape<S>;
-  constexpr uint32_t kStreams = BLOCK / 64 / WPS;  // streams per workgroup
-  constexpr uint64_t kStride = WPS * G::kBytes;    // bytes between one wave's groups
-  const uint32_t n_streams = gridDim.x * kStreams;
-  const uint32_t total = ps.chunk_end[ps.count - 1];
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t sub = wave % WPS;
-  const uint32_t lane = threadIdx.x & 63u;
-  const uint32_t cg = ps.chunk_groups;
-  uint32_t s = 0;
-  uint32_t c = blockIdx.x * kStreams + wave / WPS;
-  if (c >= total) prologue();
-  for (bool first = true; c < total; c += n_streams, first = false) {
-    if (c >= ps.chunk_end[s]) s = segment_of(ps.chunk_end, s + 1, ps.count, c);
-    const Plan& pl = ps.p[s];
-    // the chunk's groups [g0, g1), relative to the segment's first full group (a select on the
-    // chunk index, not a clamped subtraction, which has no scalar form)
-    const uint32_t j = c - (s ? ps.chunk_end[s - 1] : 0);
-    const uint32_t end = (j + 1) * cg - pl.head;
-    const uint32_t g0 = (j ? j * cg - pl.head : 0u) + sub;  // this wave's first group
-    const uint32_t g1 = end < pl.span ? end : pl.span;
-    if (g0 >= g1) {  // a short last chunk may leave a wave of its stream without a group
-      if (first) prologue();
-      continue;
-    }
-    const uint32_t cnt = (g1 - g0 + (WPS - 1)) / WPS;  // this wave's groups in the chunk
-    const uint64_t g_base = pl.g_lo;
-    char* base = pl.gbase + static_cast<uint64_t>(g0) * G::kBytes;
-    // Rotating register sets: while the body works on one group, the loads of the next AHEAD
-    // groups are in flight. No register of an outstanding load is ever copied, and inside the
-    // loops the prefetches do not depend on a branch (either would make the compiler wait
-    // for every outstanding load before the work).
-    u32x4 x[G::kRows], y[G::kRows], z[G::kRows], v[G::kRows];
-    uint32_t g = g0, i = 0;  // the current group and its index among the wave's groups
-    auto work = [&](u32x4 (&cur)[G::kRows]) {
-      body((g_base + g) * G::kVecs, cur, lane);
-      store_group<S>(base, cur, lane);
-      base += kStride;
-      g += WPS;
-      ++i;
-    };
-    auto prefetch = [&](u32x4 (&nxt)[G::kRows], uint32_t ahead) {
-      load_group<S>(nxt, base + ahead * kStride, lane);
-      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the work (the scheduler sinks it)
-    };
-    load_group<S>(x, base, lane);
-    if (first) prologue();
-    // Each steady-state loop is entered only after one full step of it has run (peeled), so
-    // that the loop is entered with the same loads and stores outstanding as its back edge:
-    // the compiler then waits for exactly the group a step needs. Entered straight from the
-    // first loads, it would merge the two states and wait, in every step, until only the
-    // newest loads were outstanding (previous stores and later prefetches included).
-    if constexpr (AHEAD == 1) {
-      auto step2 = [&]() {
-        prefetch(y, 1);
-        work(x);
-        prefetch(x, 1);
-        work(y);
-      };
-      if (i + 2 < cnt) {  // at least three groups left: steps of two that both prefetch
-        step2();
-        while (i + 2 < cnt) step2();
-      }
-      if (i + 1 < cnt) {  // two groups left
-        prefetch(y, 1);
-        work(x);
-        work(y);
-      } else {
-        work(x);
-      }
-    } else if constexpr (AHEAD == 2) {
-      auto step3 = [&]() {
-        prefetch(z, 2);
-        if constexpr (PACE > 0) __builtin_amdgcn_s_waitcnt(wait_vmcnt(PACE));
-        work(x);
-        prefetch(x, 2);
-        work(y);
-        prefetch(y, 2);
-        work(z);
-      };
-      // 2 to 4 groups left, x and y requested
-      auto last = [&]() {
-        if (i + 2 < cnt) {
-          prefetch(z, 2);
-          work(x);
-          if (i + 2 < cnt) {
-            prefetch(x, 2);
-            work(y);
-            work(z);
-            work(x);
-          } else {
-            work(y);
-            work(z);
-          }
-        } else {
-          work(x);
-          work(y);
-        }
-      };
-      if (i + 4 < cnt) {  // at least five groups left: steps of three that prefetch two ahead
-        load_group<S>(y, base + kStride, lane);
-        step3();
-        while (i + 4 < cnt) step3();
-        last();
-      } else if (i + 1 < cnt) {
-        load_group<S>(y, base + kStride, lane);
-        last();
-      } else {
-        work(x);
-      }
-    } else {
-      auto step4 = [&]() {
-        prefetch(v, 3);
-        if constexpr (PACE > 0) __builtin_amdgcn_s_waitcnt(wait_vmcnt(PACE));
-        work(x);
-        prefetch(x, 3);
-        work(y);
-        prefetch(y, 3);
-        work(z);
-        prefetch(z, 3);
-        work(v);
-      };
-      // 3 to 6 groups left, x, y and z requested
-      auto last = [&]() {
-        if (i + 3 < cnt) {
-          prefetch(v, 3);
-          work(x);
-          if (i + 3 < cnt) {
-            prefetch(x, 3);
-            work(y);
-            if (i + 3 < cnt) {
-              prefetch(y, 3);
-              work(z);
-              work(v);
-              work(x);
-              work(y);
-            } else {
-              work(z);
-              work(v);
-              work(x);
-            }
-          } else {
-            work(y);
-            work(z);
-            work(v);
-          }
-        } else {
-          work(x);
-          work(y);
-          work(z);
-        }
-      };
-      if (i + 6 < cnt) {  // at least seven groups left: steps of four that prefetch three ahead
-        load_group<S>(y, base + kStride, lane);
-        load_group<S>(z, base + 2 * kStride, lane);
-        step4();
-        while (i + 6 < cnt) step4();
-        last();
-      } else if (i + 2 < cnt) {
-        load_group<S>(y, base + kStride, lane);
-        load_group<S>(z, base + 2 * kStride, lane);
-        last();
-      } else if (i + 1 < cnt) {
-        load_group<S>(y, base + kStride, lane);
-        work(x);
-        work(y);
-      } else {
-        work(x);
-      }
-    }
-  }
-}
-
-// Calls body(plan, tile) for every edge tile of the launch, one lane per tile.
-template <int N, int BLOCK, class Body>
-__device__ __forceinline__ void for_each_edge(const Plans<N>& ps, Body body) {
-  const uint32_t n_edge = ps.edge_end[ps.count - 1];
-  const uint32_t stride = gridDim.x * BLOCK;
-  for (uint32_t j = blockIdx.x * BLOCK + threadIdx.x; j < n_edge; j += stride) {
-    const uint32_t s = segment_of(ps.edge_end, 0, ps.count, j);
-    const Plan& pl = ps.p[s];
-    const uint32_t lj = j - (s ? ps.edge_end[s - 1] : 0);
-    body(pl, lj < pl.head_nt ? pl.head_t0 + lj : pl.tail_t0 + (lj - pl.head_nt));
-  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -565,13 +222,16 @@ constexpr uint32_t table_floats() {
 // fl(lr * t), t the sum over the group's 8 probe slots of +-c (bit set: +c), pairwise; slots
 // outside [k_base, k_base + K) contribute 0. Scaling each entry once here saves the sweep a
 // multiply per element; with one probe the entry is +-fl(lr * c), the step a perturb by
-// -fl(lr * c) would apply. Thread b writes entry b of every group: the group loop and the
-// coefficient reads are uniform (scalar loads), and the sign of slot s is an XOR of the
+// -fl(lr * c) would apply. A restore probe in group fold_g (the update's own probe groups hold
+// the probe Algorithm 1 restores last) is merged into that group's entries: fl(fl(lr * t) -
+// delta), delta = +-eps_r by the probe's bit of b, so the sweep applies theta + delta - sum
+// with no per-element work of its own. Thread b writes entry b of every group: the group loop
+// and the coefficient reads are uniform (scalar loads), and the sign of slot s is an XOR of the
 // coefficient's sign bit with bit s of ~b. A workgroup of BLOCK threads builds BLOCK / 256
 // groups at a time: thread b + 256 m writes entry b of groups m, m + BLOCK / 256, ...
 template <int C, int BLOCK>
 __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32_t k_base, uint32_t K,
-                                             uint32_t n_groups, float lr) {
+                                             uint32_t n_groups, float lr, uint32_t fold_g, const Probe& fold) {
   static_assert(BLOCK % 256 == 0, "one table entry per thread");
   const uint32_t b = threadIdx.x & 255u;
   uint32_t flip[8];
@@ -586,7 +246,8 @@ __device__ __forceinline__ void build_tables(float* tab, const Coefs& cf, uint32
       const float cv = (k >= k_base && k - k_base < K) ? cf.c[k - k_base] : 0.0f;
       v[s] = __uint_as_float(__float_as_uint(cv) ^ flip[s]);
     }
-    const float t = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]))) * lr;
+    float t = (((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]))) * lr;
+    if (g == fold_g) t = t - delta(fold, b);
     if constexpr (C > 0) {
       // entry b's C / 4 float4 of copies, 256 bytes after entry b - 1's: thread b writes them
       // starting at float4 b mod (C / 4), so that the lanes of each write spread over the banks
@@ -640,23 +301,21 @@ __device__ __forceinline__ void add_group(float (&acc)[GroupShape<S>::kRows][S::
 }
 
 // Sum of the tables of probe groups 0 .. n_groups-1 for the row group: NG > 0 fixes the count
-// at compile time (one run) and leaves the last group's generator words in Wlast; NG == 0:
-// runs of 8 groups, Neumaier-compensated across runs (Wlast is not written).
+// at compile time (one run); NG == 0: runs of 8 groups, Neumaier-compensated across runs.
 template <class S, int NG, int C>
 __device__ __forceinline__ void group_sums(float (&acc)[GroupShape<S>::kRows][S::kVecElems], const float* tab,
                                            const Gen& gen, uint64_t vbase, uint32_t lane, uint32_t n_groups,
-                                           uint32_t g_first, uint32_t lane_off,
-                                           uint32_t (&Wlast)[GroupShape<S>::kRows][S::kWords]) {
+                                           uint32_t g_first, uint32_t lane_off) {
   constexpr int R = GroupShape<S>::kRows;
   static_assert(C == 0 || NG > 0, "spread tables need a fixed group count");
+  uint32_t W[R][S::kWords];
   if constexpr (NG > 0) {
-    add_group<S, true, C>(acc, tab, gen, vbase, lane, 0, g_first, lane_off, Wlast);
+    add_group<S, true, C>(acc, tab, gen, vbase, lane, 0, g_first, lane_off, W);
 #pragma unroll
     for (int g = 1; g < NG; ++g)
-      add_group<S, false, C>(acc, tab, gen, vbase, lane, g, g_first, lane_off, Wlast);
+      add_group<S, false, C>(acc, tab, gen, vbase, lane, g, g_first, lane_off, W);
   } else {
     float comp[R][S::kVecElems];
-    uint32_t W[R][S::kWords];
     for (uint32_t g0 = 0; g0 < n_groups; g0 += 8) {
       float part[R][S::kVecElems];
       add_group<S, true, 0>(part, tab, gen, vbase, lane, g0, g_first, lane_off, W);
@@ -726,12 +385,11 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
   }
 }
 
-// RESTORE: theta + eps_r z_r - lr * sum (the last probe's restore merged with the update):
-// t = fl(theta + delta_r), then t minus the sum of the lr-scaled table values. When the count of
-// groups is fixed and the restore probe lies in the last of them (Algorithm 1 restores the
-// step's last probe), its generator words are those the group sum has just produced; otherwise
-// they are generated after the group loop (keeping a middle group's words would hold them live
-// across the rest of it).
+// theta + eps_r z_r - lr * sum, the restore of probe r merged with the update. A restore probe
+// inside the update's groups (r.eps != 0, RESTORE false) is folded into its group's table (see
+// build_tables). RESTORE: a restore probe outside them, applied per element as t =
+// fl(theta + delta_r), then t minus the sum of the table values, its generator words made
+// after the group loop.
 template <class S, int NG, bool RESTORE, int N, int C, int BLOCK, int WPS, int PACE = 0, int AHEAD = 0>
 __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
                                                       uint32_t n_groups, Coefs cf, float lr, Probe r) {
@@ -740,21 +398,22 @@ __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uin
   extern __shared__ float tab_dyn[];
   __shared__ float tab_fix[NG > 0 ? table_floats<NG, C>() : 1];
   float* tab = NG > 0 ? tab_fix : tab_dyn;
+  const uint32_t g_first = k_base / 8;
+  // the table a folded restore changes (none: a group index no table has; below g_first wraps)
+  const uint32_t fold_g = !RESTORE && r.eps != 0.0f ? r.group - g_first : 0xFFFFFFFFu;
   // the tables are built while each wave's first loads are in flight (for_each_group's prologue)
-  auto build = [&]() { build_tables<C, BLOCK>(tab, cf, k_base, K, n_groups, lr); };
+  auto build = [&]() { build_tables<C, BLOCK>(tab, cf, k_base, K, n_groups, lr, fold_g, r); };
   // the lane's copy of a spread table (byte 0) and the second plane's offset (byte 2)
   const uint32_t lane_off = 4u * (threadIdx.x % (C > 0 ? C : 32)) | (1u << 16);
-  const uint32_t g_first = k_base / 8;
   constexpr int R = GroupShape<S>::kRows;
   // two groups in flight for the table counts that stream at one or two workgroups per CU;
   // one for the heavier updates, which run more waves per CU (AHEAD > 0 sets it)
   constexpr int kAhead = AHEAD ? AHEAD : C > 0 || NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
-  const bool restore_in_last = NG > 0 && r.group == g_first + static_cast<uint32_t>(NG) - 1;  // uniform
   for_each_group<S, kAhead, N, PACE, BLOCK, WPS>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
-    uint32_t Wr[R][S::kWords];  // the last group's words, then the restore probe's
-    group_sums<S, NG, C>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off, Wr);
-    if (RESTORE && !restore_in_last) group_words(gen, vbase, lane, r.group, Wr, S());
+    uint32_t Wr[R][S::kWords];  // the restore probe's words
+    group_sums<S, NG, C>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off);
+    if (RESTORE) group_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
     for (int u = 0; u < R; ++u) {
       float v[S::kVecElems];
@@ -854,61 +513,59 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
   };
   using std::integral_constant;
   using D256 = Dims<kBlock, 1>;
+  using C0 = integral_constant<int, 0>;
+  // a restore probe outside the update's groups: the per-element restore, runtime group count
+  if (w.restore && !w.fold) {
+    go(update_kernel<S, 0, true, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
+    return;
+  }
   constexpr bool bf16 = sizeof(typename S::storage) == 2;
+  using G1 = integral_constant<int, 1>;
+  using G2 = integral_constant<int, 2>;
+  using G4 = integral_constant<int, 4>;
+  using G8 = integral_constant<int, 8>;
+  using C16 = integral_constant<int, 16>;
+  using C32 = integral_constant<int, 32>;
   // The tables and launch dimensions shape_for picks for each group count: streaming bf16
-  // updates of two, four and eight groups take their own (two waves per stream; 512- and
-  // 1024-thread workgroups); everything else 256 threads.
-  auto dispatch = [&](auto restore) {
-    constexpr bool R = decltype(restore)::value;
-    using G1 = integral_constant<int, 1>;
-    using G2 = integral_constant<int, 2>;
-    using G4 = integral_constant<int, 4>;
-    using G8 = integral_constant<int, 8>;
-    using C0 = integral_constant<int, 0>;
-    using C16 = integral_constant<int, 16>;
-    using C32 = integral_constant<int, 32>;
-    switch (w.n_groups) {
-      case 1:
-        if (copies)
-          go(update_kernel<S, 1, R, N, 32, kBlock, 1>, G1{}, C32{}, D256{});
-        else
-          go(update_kernel<S, 1, R, N, 0, kBlock, 1>, G1{}, C0{}, D256{});
-        break;
-      case 2:
-        if (!copies)
-          go(update_kernel<S, 2, R, N, 0, kBlock, 1>, G2{}, C0{}, D256{});
-        else if constexpr (!bf16)
-          go(update_kernel<S, 2, R, N, 32, kBlock, 1>, G2{}, C32{}, D256{});
-        else if constexpr (R)
-          go(update_kernel<S, 2, R, N, 32, 256, 2>, G2{}, C32{}, Dims<256, 2>{});
-        else
-          go(update_kernel<S, 2, R, N, 32, 512, 2>, G2{}, C32{}, Dims<512, 2>{});
-        break;
-      case 4:
-        if (!copies || !bf16)
-          go(update_kernel<S, 4, R, N, 0, kBlock, 1>, G4{}, C0{}, D256{});
-        else if constexpr (R)
-          go(update_kernel<S, 4, R, N, 16, 512, 1>, G4{}, C16{}, Dims<512, 1>{});
-        else
-          go(update_kernel<S, 4, R, N, 32, 1024, 1>, G4{}, C32{}, Dims<1024, 1>{});
-        break;
-      case 8:
-        if (!copies || !bf16)
-          go(update_kernel<S, 8, R, N, 0, kBlock, 1>, G8{}, C0{}, D256{});
-        else if constexpr (R)
-          go(update_kernel<S, 8, R, N, 16, 512, 1>, G8{}, C16{}, Dims<512, 1>{});
-        else
-          go(update_kernel<S, 8, R, N, 16, 1024, 1>, G8{}, C16{}, Dims<1024, 1>{});
-        break;
-      default:
-        go(update_kernel<S, 0, R, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
-        break;
-    }
-  };
-  if (w.restore)
-    dispatch(std::true_type{});
-  else
-    dispatch(std::false_type{});
+  // updates of two, four and eight groups take their own (two waves per stream; 1024-thread
+  // workgroups); everything else 256 threads. A folded restore runs these same kernels.
+  switch (w.n_groups) {
+    case 1:
+      if (copies)
+        go(update_kernel<S, 1, false, N, 32, kBlock, 1>, G1{}, C32{}, D256{});
+      else
+        go(update_kernel<S, 1, false, N, 0, kBlock, 1>, G1{}, C0{}, D256{});
+      break;
+    case 2:
+      if (!copies)
+        go(update_kernel<S, 2, false, N, 0, kBlock, 1>, G2{}, C0{}, D256{});
+      else if constexpr (!bf16)
+        go(update_kernel<S, 2, false, N, 32, kBlock, 1>, G2{}, C32{}, D256{});
+      else
+        go(update_kernel<S, 2, false, N, 32, 512, 2>, G2{}, C32{}, Dims<512, 2>{});
+      break;
+    case 4:
+      if constexpr (bf16) {
+        if (copies) {
+          go(update_kernel<S, 4, false, N, 32, 1024, 1>, G4{}, C32{}, Dims<1024, 1>{});
+          break;
+        }
+      }
+      go(update_kernel<S, 4, false, N, 0, kBlock, 1>, G4{}, C0{}, D256{});
+      break;
+    case 8:
+      if constexpr (bf16) {
+        if (copies) {
+          go(update_kernel<S, 8, false, N, 16, 1024, 1>, G8{}, C16{}, Dims<1024, 1>{});
+          break;
+        }
+      }
+      go(update_kernel<S, 8, false, N, 0, kBlock, 1>, G8{}, C0{}, D256{});
+      break;
+    default:
+      go(update_kernel<S, 0, false, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
+      break;
+  }
 }
 
 // One contiguous tensor.

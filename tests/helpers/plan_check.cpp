@@ -300,6 +300,19 @@ static void check_validation() {
   CHECK(make_update_sweep(w, 0, 16, c.data(), 1e-3f, &r0) == ZO_OK && !w.restore, "zero restore");
   CHECK(make_update_sweep(w, 0, 16, c.data(), 1e-3f, &r1) == ZO_OK && w.restore && w.r.group == 1 && w.r.bit == 7,
         "restore probe");
+  // the restore is merged into a table exactly when its probe group is one of the update's
+  CHECK(w.fold, "restore of the last probe folds");
+  CHECK(make_update_sweep(w, 0, 16, c.data(), 1e-3f, &r0) == ZO_OK && !w.fold, "zero restore does not fold");
+  const Probe r_in = make_probe(3, 1e-3f), r_below = make_probe(7, 1e-3f), r_above = make_probe(40, 1e-3f);
+  CHECK(make_update_sweep(w, 0, 16, c.data(), 1e-3f, &r_in) == ZO_OK && w.fold, "restore in the first group");
+  CHECK(make_update_sweep(w, 8, 16, c.data(), 1e-3f, &r_below) == ZO_OK && w.restore && !w.fold,
+        "restore below the update's groups");
+  CHECK(make_update_sweep(w, 3, 13, c.data(), 1e-3f, &r1) == ZO_OK && w.fold, "restore in a partly used group");
+  CHECK(make_update_sweep(w, 0, 16, c.data(), 1e-3f, &r_above) == ZO_OK && w.restore && !w.fold,
+        "restore above the update's groups");
+  const Probe r_top = make_probe(0xFFFFFFFFu, 1e-3f);
+  CHECK(make_update_sweep(w, 0xFFFFFFC0u, 64, c.data(), 1e-3f, &r_top) == ZO_OK && w.fold, "restore of probe 2^32 - 1");
+  CHECK(make_update_sweep(w, 0, 64, c.data(), 1e-3f, &r_top) == ZO_OK && !w.fold, "far restore does not fold");
   CHECK(make_update_sweep(w, 5, 1000, c.data(), 1e-3f, nullptr) == ZO_OK && w.n_groups == 126, "groups of 5..1004");
   const uint32_t kb = 9;
   const Sweep two = perturb_sweep(1, 1e-3f, &kb, -2e-3f);

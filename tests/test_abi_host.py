@@ -49,13 +49,18 @@ def test_calibration_library_exports_its_header():
         pytest.fail("libzo_calib.so is not built (run __graft_entry__.build())")
     calib = ctypes.CDLL(path)
     names = _declared_functions("zo_calib.h")
-    assert names == ["zo_calib_rmw"]
+    assert names == ["zo_calib_rmw", "zo_calib_rmw_shape"]
     calib.zo_calib_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p]
+    calib.zo_calib_rmw_shape.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32,
+                                         ctypes.c_void_p]
     # validation returns before any HIP call
     assert calib.zo_calib_rmw(None, 0, 1, None) == 0
     assert calib.zo_calib_rmw(None, 16, 1, None) == -1
     assert calib.zo_calib_rmw(ctypes.c_void_p(0x1008), 16, 1, None) == -2
     assert calib.zo_calib_rmw(ctypes.c_void_p(0x1000), 24, 1, None) == -2
+    assert calib.zo_calib_rmw_shape(None, 16, 1, 3, None) == -1
+    assert calib.zo_calib_rmw_shape(ctypes.c_void_p(0x1000), 16, 1, 4, None) == -2
+    assert calib.zo_calib_rmw_shape(ctypes.c_void_p(0x1000), 1 << 41, 1, 0, None) == -2
 
 
 def test_header_constants_match_binding():
