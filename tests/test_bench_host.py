@@ -2,7 +2,6 @@
 lookup of committed profile counters, and the CPU oracle baseline on a tiny budget."""
 
 import glob
-import hashlib
 import json
 import os
 import subprocess
@@ -35,14 +34,13 @@ def test_per_tensor_layout_needs_an_opt_workload():
 def test_committed_counters_match_the_sweep_source():
     """Every profile summary carries a counters-json line for the current sweep source, and the
     bench finds it by workload, K, dtype and layout (so `traffic` is not null)."""
-    src = os.path.join(ROOT, "paper_2609_38095_amd", "csrc", "zo_sweep.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    digest = bench.sweep_source_digest()
     found = []
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         lines = [ln for ln in open(path) if ln.startswith("counters-json:")]
         assert len(lines) == 1, path
         d = json.loads(lines[0].split(":", 1)[1])
-        assert d["source_sha256"] == digest, f"{path} was taken with another zo_sweep.hip"
+        assert d["source_sha256"] == digest, f"{path} was taken with other sweep sources"
         got = bench.measured_counters(d["workload"], d["K"], d["dtype"], d.get("layout", "flat"))
         assert got == d
         sweep = 2 * 2 * workloads.WORKLOADS[d["workload"]].n
