@@ -297,11 +297,11 @@ class Sweeps:
         run("zo_update_restore", lambda: self.update_restore(c, step, K - 1, w.eps))
 
 
-def rmw_ceiling(sw, b, launches=4):
+def rmw_ceiling(sw, b, launches=6):
     """The plain in-place read-modify-write ceiling of the flat buffer: the fastest of the
-    XOR sweep's four shapes (the sweeps' own streaming loop, grid-stride or one chunk per
-    wave, unpaced or paced), each timed over `launches` launches (an even number of XOR
-    passes leaves the weights as they were)."""
+    XOR sweep's eight shapes (the sweeps' own streaming loop, grid-stride or one chunk per
+    wave, unpaced or paced, two or three row groups in flight), each timed over `launches`
+    launches (an even number of XOR passes leaves the weights as they were)."""
     import ctypes
 
     import numpy as np
@@ -311,7 +311,8 @@ def rmw_ceiling(sw, b, launches=4):
                                          ctypes.c_void_p]
     sptr = ctypes.c_void_p(sw.stream.cuda_stream)
     buf_bytes = sw.w.n * b - (sw.w.n * b) % 16
-    names = {0: "grid-stride", 1: "one chunk per wave", 2: "grid-stride, paced", 3: "one chunk per wave, paced"}
+    base = {0: "grid-stride", 1: "one chunk per wave", 2: "grid-stride, paced", 3: "one chunk per wave, paced"}
+    names = {flags | ahead: name + (", three ahead" if ahead else "") for ahead in (0, 4) for flags, name in base.items()}
     shapes = {}
     for shape, name in names.items():
         def rmw():

@@ -29,9 +29,10 @@ int zo_calib_rmw(void* p, uint64_t bytes, uint32_t key, void* stream);
 
 /* zo_calib_rmw in another launch shape, so that the ceiling can be taken as the fastest of
  * several: shape bit 0 = one 32 KiB chunk per wave (a grid sized to the buffer instead of
- * grid-stride), bit 1 = paced (each step of three groups first waits until at most four memory
- * operations of the wave are outstanding). shape 0 is zo_calib_rmw. Returns as zo_calib_rmw,
- * and -2 also for shape bits above bit 1 (nothing launched). */
+ * grid-stride), bit 1 = paced (each step of the loop first waits until at most four memory
+ * operations of the wave are outstanding, six with three groups in flight), bit 2 = the loads
+ * of three row groups in flight instead of two. shape 0 is zo_calib_rmw. Returns as zo_calib_rmw, and -2 also for shape
+ * bits above bit 2 (nothing launched). */
 int zo_calib_rmw_shape(void* p, uint64_t bytes, uint32_t key, uint32_t shape, void* stream);
 
 #ifdef __cplusplus

@@ -4,9 +4,9 @@
 // row groups of two rows of 64 lanes x 16 bytes, non-temporal loads and stores, chunks of up
 // to 32 KiB per wave with the loads of the next two groups in flight, one workgroup of 256
 // threads per CU at a time (dynamic LDS), and the sweeps' launch plan (zo_plan.cpp). Shapes:
-// grid-stride over up to 65,536 workgroups or one chunk per wave, unpaced or paced at four
-// outstanding memory operations, as the sweeps are launched. Two calls with the same key
-// restore the buffer exactly.
+// grid-stride over up to 65,536 workgroups or one chunk per wave, unpaced or paced (at four
+// outstanding memory operations with two groups in flight, six with three), as the sweeps are
+// launched. Two calls with the same key restore the buffer exactly.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -18,13 +18,13 @@ namespace {
 
 using namespace zo;
 
-template <int PACE>
+template <int AHEAD, int PACE>
 __global__ __launch_bounds__(kBlock) void xor_sweep(Plans<1> ps, uint32_t key) {
   extern __shared__ uint32_t occupancy_pad[];  // dynamic LDS only limits workgroups per CU
   if (ps.count == 0xFFFFFFFFu) occupancy_pad[threadIdx.x] = 0;  // never taken (count is 1)
   const u32x4 k = {key, key, key, key};
   constexpr int R = GroupShape<BF16>::kRows;
-  for_each_group<BF16, 2, 1, PACE, kBlock, 1>(
+  for_each_group<BF16, AHEAD, 1, PACE, kBlock, 1>(
       ps,
       [&](uint64_t, u32x4 (&d)[R], uint32_t) {
 #pragma unroll
@@ -48,22 +48,25 @@ __global__ __launch_bounds__(kBlock) void xor_sweep(Plans<1> ps, uint32_t key) {
 
 }  // namespace
 
-// shape: bit 0 one chunk per wave, bit 1 paced. 0 on success; -1 for a null pointer with
-// bytes > 0; -2 when p is not 16-byte aligned, bytes is not a multiple of 16 or reaches 2^41,
-// or shape has other bits; -4 when the launch fails. Asynchronous on `stream`.
+// shape: bit 0 one chunk per wave, bit 1 paced, bit 2 three groups in flight instead of two.
+// 0 on success; -1 for a null pointer with bytes > 0; -2 when p is not 16-byte aligned, bytes
+// is not a multiple of 16 or reaches 2^41, or shape has other bits; -4 when the launch fails.
+// Asynchronous on `stream`.
 extern "C" int zo_calib_rmw_shape(void* p, uint64_t bytes, uint32_t key, uint32_t shape, void* stream) {
   if (bytes == 0) return 0;
   if (p == nullptr) return -1;
   if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0 || (bytes & 15u) != 0) return -2;
   if (bytes / 2 >= ZO_N_MAX) return -2;
-  if (shape & ~3u) return -2;
+  if (shape & ~7u) return -2;
   const bool one_chunk_per_wave = shape & 1u, paced = shape & 2u;
   const Shape sh{static_cast<uint32_t>(kMaxChunkBytes / (kGroupElems * 2)), 1, one_chunk_per_wave ? 1u : 0u};
   Plans<1> ps{};
   ps.chunk_groups = sh.chunk_groups;
-  add_plan(ps, make_plan(p, 0, bytes / 2, 2, sh.chunk_groups));
+  add_plan(ps, make_plan(p, 0, bytes / 2, 2, sh.chunk_groups), 2, streams_per_block(sh));
   const size_t pad = occupancy_lds(sh.blocks_per_cu, 0);
-  auto kernel = paced ? xor_sweep<4> : xor_sweep<0>;
+  const bool three = shape & 4u;
+  // paced: the step's own prefetch and the previous step's last stores stay outstanding
+  auto kernel = three ? (paced ? xor_sweep<3, 6> : xor_sweep<3, 0>) : (paced ? xor_sweep<2, 4> : xor_sweep<2, 0>);
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
                             static_cast<int>(pad));
   (void)hipGetLastError();

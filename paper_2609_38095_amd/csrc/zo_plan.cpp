@@ -73,8 +73,8 @@ Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint32_t 
     if (g_lo < g_hi) {  // g_hi - g_lo < 2^30: n < ZO_N_MAX is checked first
       pl.g_lo = g_lo;
       pl.span = static_cast<uint32_t>(g_hi - g_lo);
-      pl.head = static_cast<uint32_t>(g_lo % chunk_groups);
       pl.gbase = reinterpret_cast<char*>(addr + static_cast<uintptr_t>((g_lo * kGroupElems - pl.lo) * elem));
+      pl.head = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(pl.gbase) / (kGroupElems * elem) % chunk_groups);
       head_end = g_lo * kGroupElems;
       tail_begin = g_hi * kGroupElems;
     }
@@ -90,7 +90,7 @@ Plan make_plan(void* params, uint64_t offset, uint64_t n, size_t elem, uint32_t 
   return pl;
 }
 
-// Chunks that meet a plan's full row groups (fewer than 2^30 + 2).
+// Chunk slots of a plan, the leading empty ones included (fewer than 2^30 + 2 + 16).
 uint32_t plan_chunks(const Plan& pl, uint32_t chunk_groups) {
   return pl.span ? static_cast<uint32_t>(ceil_div(static_cast<uint64_t>(pl.head) + pl.span, chunk_groups)) : 0u;
 }

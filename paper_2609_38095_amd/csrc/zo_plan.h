@@ -29,10 +29,16 @@ constexpr uint64_t kStreamBytes = 256ull << 20;    // sweeps at least this large
 
 // One segment: global elements [lo, hi) stored from `base` (the address of global element lo).
 // The `span` full row groups from global group g_lo (stored from `gbase`) take the vector
-// path, in chunks of up to `chunk_groups` groups aligned to multiples of chunk_groups in the
-// global group index: the segment's first chunk starts `head` = g_lo mod chunk_groups groups
-// before g_lo. The edge tiles [head_t0, +head_nt) and [tail_t0, +tail_nt) (fewer than 1024
-// elements at each end) take the element-wise path. The kernels walk chunks and groups with
+// path, in chunk slots of `chunk_groups` groups whose boundaries sit at multiples of
+// chunk_groups x the group's bytes in memory (as far as gbase's alignment allows): slot j
+// holds the segment's groups [j chunk_groups - head, (j + 1) chunk_groups - head) clipped to
+// [0, span). make_plan sets head = (gbase / group bytes) mod chunk_groups; add_plan adds whole
+// empty slots in front (head grows by multiples of chunk_groups) so that a launch's chunk index
+// and the memory index of the chunk agree modulo the streams of a workgroup, i.e. each
+// workgroup streams one aligned block of memory (OPT-13B bf16 perturb: 7.65 ms with the
+// workgroups' 128 KiB blocks aligned, 8.0-8.25 ms shifted by one to three 32 KiB chunks). The
+// edge tiles [head_t0, +head_nt) and [tail_t0, +tail_nt) (fewer than 1024 elements at each
+// end) take the element-wise path. The kernels walk chunks and groups with
 // 32-bit indices relative to the segment (compares of 64-bit indices need a vector register
 // on gfx950, and writing one that a pending store still reads makes the wave wait for that
 // store); a segment stays below 2^30 row groups (n < ZO_N_MAX) and a launch below 2^31 chunks.
@@ -118,11 +124,22 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w);
 size_t occupancy_lds(uint32_t cap, size_t static_lds);
 void set_max_blocks(uint32_t max_blocks);
 
+// Streams (chunks in flight at once) of one workgroup of a launch shape.
+inline uint32_t streams_per_block(const Shape& sh) { return sh.block / 64 / sh.wps; }
+
+// Appends a plan to a launch: its chunk slots start at the launch's next chunk index after
+// (memory chunk of its first full group - that index) mod `streams` empty slots, so that every
+// chunk's launch index is congruent to its memory chunk index modulo `streams`.
 template <int N>
-void add_plan(Plans<N>& ps, const Plan& pl) {
+void add_plan(Plans<N>& ps, Plan pl, size_t elem, uint32_t streams) {
   const uint32_t s = ps.count++;
+  const uint32_t prev = s ? ps.chunk_end[s - 1] : 0;
+  if (pl.span && streams > 1) {
+    const uint64_t mem_chunk = reinterpret_cast<uintptr_t>(pl.gbase) / (kGroupElems * elem) / ps.chunk_groups;
+    pl.head += static_cast<uint32_t>((mem_chunk % streams + streams - prev % streams) % streams) * ps.chunk_groups;
+  }
   ps.p[s] = pl;
-  ps.chunk_end[s] = (s ? ps.chunk_end[s - 1] : 0) + plan_chunks(pl, ps.chunk_groups);
+  ps.chunk_end[s] = prev + plan_chunks(pl, ps.chunk_groups);
   ps.edge_end[s] = (s ? ps.edge_end[s - 1] : 0) + pl.head_nt + pl.tail_nt;
 }
 
@@ -142,21 +159,24 @@ uint32_t plans_grid(const Plans<N>& ps, const Shape& sh) {
 // A list of tensors in launches of up to N plans: calls launch(plans) for every batch.
 // Segments with n = 0 are skipped; a segment without full row groups is planned in pieces of
 // kPieceElems; a batch is closed before its chunk or edge-tile count would reach 2^31.
+// `streams`: the streams of one workgroup of the launches (the chunk alignment of add_plan).
 // Returns the first status launch() returns other than ZO_OK, else ZO_OK. The list must have
 // passed check_segments.
 template <int N, class Launch>
-int plan_segments(const zo_segment* segs, uint32_t n_segs, size_t elem, uint32_t chunk_groups, Launch launch) {
+int plan_segments(const zo_segment* segs, uint32_t n_segs, size_t elem, uint32_t chunk_groups, uint32_t streams,
+                  Launch launch) {
   Plans<N> ps{};
   ps.chunk_groups = chunk_groups;
   auto add = [&](const Plan& pl) {
-    if (ps.count && (ps.chunk_end[ps.count - 1] + static_cast<uint64_t>(plan_chunks(pl, chunk_groups)) >=
+    // the plan's chunks plus up to streams - 1 alignment slots
+    if (ps.count && (ps.chunk_end[ps.count - 1] + static_cast<uint64_t>(plan_chunks(pl, chunk_groups)) + streams >=
                          kMaxLaunchChunks ||
                      ps.edge_end[ps.count - 1] + static_cast<uint64_t>(pl.head_nt) + pl.tail_nt >= kMaxLaunchEdges)) {
       const int rc = launch(ps);  // keep a launch's chunk and edge counts 32-bit
       if (rc != ZO_OK) return rc;
       ps.count = 0;
     }
-    add_plan(ps, pl);
+    add_plan(ps, pl, elem, streams);
     if (ps.count == N) {
       const int rc = launch(ps);
       if (rc != ZO_OK) return rc;

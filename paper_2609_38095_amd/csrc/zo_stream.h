@@ -190,16 +190,17 @@ __device__ __forceinline__ void for_each_group(const Plans<N>& ps, Body body, Pr
   for (bool first = true; c < total; c += n_streams, first = false) {
     if (c >= ps.chunk_end[s]) s = segment_of(ps.chunk_end, s + 1, ps.count, c);
     const Plan& pl = ps.p[s];
-    // the chunk's groups [g0, g1), relative to the segment's first full group (a select on the
-    // chunk index, not a clamped subtraction, which has no scalar form)
+    // slot j of the segment holds groups [j cg - head, (j + 1) cg - head) clipped to [0, span)
+    // (relative to the segment's first full group); leading alignment slots hold none
     const uint32_t j = c - (s ? ps.chunk_end[s - 1] : 0);
-    const uint32_t end = (j + 1) * cg - pl.head;
-    const uint32_t g0 = (j ? j * cg - pl.head : 0u) + sub;  // this wave's first group
-    const uint32_t g1 = end < pl.span ? end : pl.span;
-    if (g0 >= g1) {  // a short last chunk may leave a wave of its stream without a group
+    const uint32_t a = j * cg, b = (j + 1) * cg, top = pl.head + pl.span;
+    const uint32_t lo = a > pl.head ? a : pl.head, hi = b < top ? b : top;
+    if (lo + sub >= hi) {  // an alignment slot, or a short chunk without a group for this wave
       if (first) prologue();
       continue;
     }
+    const uint32_t g0 = lo - pl.head + sub;  // this wave's first group
+    const uint32_t g1 = hi - pl.head;
     const uint32_t cnt = (g1 - g0 + (WPS - 1)) / WPS;  // this wave's groups in the chunk
     const uint64_t g_base = pl.g_lo;
     char* base = pl.gbase + static_cast<uint64_t>(g0) * G::kBytes;

@@ -577,7 +577,8 @@ int run_one(void* params, uint64_t offset, uint64_t n, uint64_t seed, uint32_t s
   const zo_segment seg{params, offset, n};
   (void)hipGetLastError();
   // one launch (several only for a tensor of more than kPieceElems weights without full row groups)
-  return plan_segments<1>(&seg, 1, sizeof(typename S::storage), sh.chunk_groups, [&](const Plans<1>& ps) {
+  return plan_segments<1>(&seg, 1, sizeof(typename S::storage), sh.chunk_groups, streams_per_block(sh),
+                          [&](const Plans<1>& ps) {
     launch_sweep<S>(ps, gen, w, sh, st);
     return launch_status();
   });
@@ -606,7 +607,7 @@ int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_
   const Shape sh = shape_for(total, sizeof(typename S::storage), w);
   (void)hipGetLastError();
   return plan_segments<kSegsPerLaunch>(segs, n_segs, sizeof(typename S::storage), sh.chunk_groups,
-                                       [&](const Plans<kSegsPerLaunch>& ps) {
+                                       streams_per_block(sh), [&](const Plans<kSegsPerLaunch>& ps) {
                                          launch_sweep<S>(ps, gen, w, sh, st);
                                          return launch_status();
                                        });

@@ -49,41 +49,46 @@ static uint64_t rnd() {
   return z ^ (z >> 31);
 }
 
-// The kernels' walk over one plan's chunks (for_each_group): chunk j of the segment covers
-// groups [j cg - head, (j + 1) cg - head) clipped to [0, span); wave `sub` of a stream of
-// `wps` waves takes every wps-th of them. All of it in 32-bit arithmetic, as on the device;
-// the 64-bit shadow checks that nothing wraps. Returns the groups visited per chunk.
+// The kernels' walk over one plan's chunk slots (for_each_group): slot j of the segment holds
+// groups [j cg - head, (j + 1) cg - head) clipped to [0, span), and only slots wholly before
+// the first group (alignment slots) are empty; wave `sub` of a stream of `wps` waves takes
+// every wps-th group of a slot. All of it in 32-bit arithmetic, as on the device; the 64-bit
+// shadow checks that nothing wraps and that the groups are covered exactly once.
 static void check_chunk_walk(const Plan& pl, uint32_t cg, uint32_t wps, const char* what) {
   const uint32_t chunks = plan_chunks(pl, cg);
   if (pl.span == 0) {
     CHECK(chunks == 0, "%s: chunks without full groups", what);
     return;
   }
-  CHECK(pl.head < cg, "%s: head %u >= chunk groups %u", what, pl.head, cg);
-  CHECK((u128)chunks * cg <= (u128)pl.head + pl.span + cg, "%s: chunk count", what);
-  // every chunk when few, else the first and last thousand and a random sample
+  const u128 top64 = (u128)pl.head + pl.span;
+  CHECK(top64 + cg < ((u128)1 << 32), "%s: slot arithmetic wraps", what);
+  CHECK((u128)chunks * cg >= top64 && (u128)(chunks - 1) * cg < top64, "%s: chunk count", what);
+  // every slot when few, else the leading ones, the first and last thousand and a sample
   std::vector<uint32_t> js;
   if (chunks <= 20000) {
     for (uint32_t j = 0; j < chunks; ++j) js.push_back(j);
   } else {
-    for (uint32_t j = 0; j < 1000; ++j) js.push_back(j);
+    for (uint32_t j = 0; j < 1000 + pl.head / cg; ++j) js.push_back(j);
     for (uint32_t j = chunks - 1000; j < chunks; ++j) js.push_back(j);
     for (int i = 0; i < 2000; ++i) js.push_back(static_cast<uint32_t>(rnd() % chunks));
   }
   uint64_t covered = 0;
   for (uint32_t j : js) {
-    const uint64_t end64 = (uint64_t)(j + 1) * cg - pl.head;
-    const uint64_t start64 = j ? (uint64_t)j * cg - pl.head : 0;
-    CHECK(end64 < (1ull << 32), "%s: chunk end wraps", what);
-    const uint32_t end = (j + 1) * cg - pl.head;
-    const uint32_t g0c = j ? j * cg - pl.head : 0u;
-    const uint32_t g1 = end < pl.span ? end : pl.span;
-    CHECK(g0c == start64 && g0c < g1, "%s: chunk %u empty or misplaced", what, j);
-    CHECK(j + 1 == chunks ? g1 == pl.span : g1 == end, "%s: chunk %u end", what, j);
+    const u128 a64 = (u128)j * cg, b64 = a64 + cg;
+    const u128 lo64 = a64 > pl.head ? a64 : (u128)pl.head, hi64 = b64 < top64 ? b64 : top64;
+    // the device's 32-bit form
+    const uint32_t a = j * cg, b = (j + 1) * cg, top = pl.head + pl.span;
+    const uint32_t lo = a > pl.head ? a : pl.head, hi = b < top ? b : top;
+    CHECK(lo == lo64 && hi == hi64, "%s: slot %u bounds", what, j);
+    if (lo >= hi) {
+      CHECK(b64 <= pl.head, "%s: slot %u empty after the first group", what, j);
+      continue;
+    }
+    const uint32_t g0c = lo - pl.head, g1 = hi - pl.head;
     uint64_t in_chunk = 0;
     for (uint32_t sub = 0; sub < wps; ++sub) {
+      if (lo + sub >= hi) continue;
       const uint32_t g0 = g0c + sub;
-      if (g0 >= g1) continue;
       const uint32_t cnt = (g1 - g0 + (wps - 1)) / wps;
       const uint64_t last = (uint64_t)g0 + (uint64_t)wps * (cnt - 1);
       CHECK(last < g1 && last + wps >= g1, "%s: wave %u of chunk %u", what, sub, j);
@@ -95,6 +100,34 @@ static void check_chunk_walk(const Plan& pl, uint32_t cg, uint32_t wps, const ch
   }
   if (chunks <= 20000) CHECK(covered == pl.span, "%s: chunks cover %llu of %u groups", what,
                              (unsigned long long)covered, pl.span);
+}
+
+// The memory chunk of a plan's slot j: slot boundaries sit at multiples of cg groups in memory.
+static uint64_t mem_chunk_of(const Plan& pl, size_t elem, uint32_t cg, uint32_t j) {
+  const uint64_t g_mem = reinterpret_cast<uintptr_t>(pl.gbase) / (kGroupElems * elem);  // memory group of group 0
+  return (g_mem + (uint64_t)j * cg - pl.head) / cg;
+}
+
+// In a launch, every non-empty slot's launch chunk index is congruent to its memory chunk
+// index modulo the streams of a workgroup, and slot boundaries sit at memory chunk boundaries
+// (where the first full group sits at a group boundary in memory).
+template <int N>
+static void check_alignment(const Plans<N>& ps, size_t elem, uint32_t streams, const char* what) {
+  const uint32_t cg = ps.chunk_groups;
+  for (uint32_t s = 0; s < ps.count; ++s) {
+    const Plan& pl = ps.p[s];
+    if (!pl.span) continue;
+    const uint32_t first = pl.head / cg, prev = s ? ps.chunk_end[s - 1] : 0;
+    CHECK(pl.head < streams * cg, "%s: segment %u has %u alignment slots", what, s, first);
+    const uint64_t g_mem = reinterpret_cast<uintptr_t>(pl.gbase) / (kGroupElems * elem);
+    CHECK(pl.head % cg == g_mem % cg, "%s: segment %u slot boundaries", what, s);
+    for (uint32_t j : {first, first + 1, ps.chunk_end[s] - prev - 1}) {
+      if (prev + j >= ps.chunk_end[s]) continue;
+      CHECK((prev + j) % streams == mem_chunk_of(pl, elem, cg, j) % streams,
+            "%s: segment %u slot %u: launch chunk %u, memory chunk %llu", what, s, j, prev + j,
+            (unsigned long long)mem_chunk_of(pl, elem, cg, j));
+    }
+  }
 }
 
 // make_plan's split of [offset, offset + n) into edge tiles and full row groups.
@@ -112,8 +145,8 @@ static void check_plan(uintptr_t addr, uint64_t offset, uint64_t n, size_t elem,
     const u128 f0 = (u128)pl.g_lo * kGroupElems, f1 = f0 + (u128)pl.span * kGroupElems;
     CHECK(f0 >= lo && f0 - lo < kGroupElems, "%s: first full group", what);
     CHECK(f1 <= hi && hi - f1 < kGroupElems, "%s: last full group", what);
-    CHECK(pl.head == pl.g_lo % cg, "%s: head", what);
     const uintptr_t gb = reinterpret_cast<uintptr_t>(pl.gbase);
+    CHECK(pl.head == gb / (kGroupElems * elem) % cg, "%s: head", what);
     CHECK(gb == addr + (uintptr_t)((f0 - lo) * elem), "%s: gbase", what);
     CHECK((gb & 15u) == 0, "%s: gbase misaligned", what);
     head_end = f0;
@@ -147,12 +180,17 @@ static void check_plan(uintptr_t addr, uint64_t offset, uint64_t n, size_t elem,
 // A tensor through plan_segments (one plan per launch, as zo_perturb launches one tensor):
 // the plans' element ranges, in order, partition [offset, offset + n), each plan as check_plan
 // requires, and every launch stays below 2^31 edge tiles.
-static void check_pieces(uintptr_t addr, uint64_t offset, uint64_t n, size_t elem, uint32_t cg) {
+static void check_pieces(uintptr_t addr, uint64_t offset, uint64_t n, size_t elem, uint32_t cg,
+                         uint32_t streams = 4) {
   const zo_segment seg{reinterpret_cast<void*>(addr), offset, n};
   u128 next = offset;
   size_t plans = 0;
-  const int rc = plan_segments<1>(&seg, 1, elem, cg, [&](const Plans<1>& ps) {
+  const int rc = plan_segments<1>(&seg, 1, elem, cg, streams, [&](const Plans<1>& ps) {
     const Plan& pl = ps.p[0];
+    check_alignment(ps, elem, streams, "pieces");
+    if (pl.span) {
+      for (uint32_t wps : {1u, 2u}) check_chunk_walk(pl, cg, wps, "launched piece");
+    }
     CHECK(ps.count == 1 && pl.lo == next, "pieces out of order at %llu", (unsigned long long)pl.lo);
     CHECK((uint64_t)ps.edge_end[0] < kMaxLaunchEdges, "launch of %u edge tiles", ps.edge_end[0]);
     CHECK((u128)ps.edge_end[0] == (u128)pl.head_nt + pl.tail_nt, "edge count");
@@ -191,7 +229,7 @@ static void check_plans() {
     for (uint32_t cg : {1u, 8u, 16u})
       for (uint64_t n : {ZO_N_MAX - 1, ZO_N_MAX - 1024, (1ull << 39) + 5, (1ull << 31) + 777})
         for (uint64_t off : {(uint64_t)0, (uint64_t)1023, (uint64_t)(1ull << 33) + 1, top - n, top - n - 5000}) {
-          check_pieces(A, off, n, elem, cg);
+          check_pieces(A, off, n, elem, cg, 16);
           check_pieces(A + elem, off, n, elem, cg);
         }
   // random cases
@@ -201,7 +239,9 @@ static void check_plans() {
     const uint64_t n = 1 + rnd() % (1ull << (rnd() % 24 + 1));
     uint64_t off = rnd() >> (rnd() % 64);
     if (off > top - n) off = top - n;
-    check_pieces(A + 2 * (rnd() % 64) * (elem / 2), off, n, elem, cg);
+    // bases anywhere in a 128 KiB window, so that the alignment slots take every value
+    const uint32_t streams = 1u << (rnd() % 5);
+    check_pieces(A + (rnd() % 65536) * elem, off, n, elem, cg, streams);
   }
 }
 
@@ -211,15 +251,19 @@ static void check_batches() {
   uint64_t g = 0;
   for (int i = 0; i < 150; ++i) {
     const uint64_t n = i % 17 == 5 ? 0 : 1 + rnd() % 5000000;
-    segs.push_back({reinterpret_cast<void*>(0x7f0000000000ull + (uint64_t)i * (1ull << 26)), g, n});
+    // most tensors 16-byte aligned relative to their global offset, at any 16-byte position
+    // of a 128 KiB window (so the alignment slots take every value), some not aligned at all
+    const uint64_t at = (i % 7 == 3 ? 2 : (2 * g) % 16) + 16 * (rnd() % 8192);
+    segs.push_back({reinterpret_cast<void*>(0x7f0000000000ull + (uint64_t)i * (1ull << 26) + at), g, n});
     g += n + rnd() % 3;
   }
   CHECK(check_segments(segs.data(), (uint32_t)segs.size(), ZO_BF16) == ZO_OK, "disjoint segments rejected");
   std::vector<size_t> seen;
   size_t launches = 0;
-  int rc = plan_segments<kSegsPerLaunch>(segs.data(), (uint32_t)segs.size(), 2, 16, [&](const Plans<kSegsPerLaunch>& ps) {
+  int rc = plan_segments<kSegsPerLaunch>(segs.data(), (uint32_t)segs.size(), 2, 16, 4, [&](const Plans<kSegsPerLaunch>& ps) {
     ++launches;
     CHECK(ps.count >= 1 && ps.count <= kSegsPerLaunch, "batch of %u segments", ps.count);
+    check_alignment(ps, 2, 4, "batch");
     for (uint32_t s = 0; s < ps.count; ++s) {
       for (size_t i = 0; i < segs.size(); ++i)
         if (segs[i].params == ps.p[s].base && segs[i].n) seen.push_back(i);
@@ -245,7 +289,7 @@ static void check_batches() {
   CHECK(check_segments(big.data(), 40, ZO_BF16) == ZO_OK, "huge disjoint segments rejected");
   size_t total = 0;
   launches = 0;
-  rc = plan_segments<kSegsPerLaunch>(big.data(), 40, 2, 16, [&](const Plans<kSegsPerLaunch>& ps) {
+  rc = plan_segments<kSegsPerLaunch>(big.data(), 40, 2, 16, 16, [&](const Plans<kSegsPerLaunch>& ps) {
     ++launches;
     CHECK((uint64_t)ps.chunk_end[ps.count - 1] < kMaxLaunchChunks, "launch of %u chunks", ps.chunk_end[ps.count - 1]);
     total += ps.count;
@@ -254,7 +298,7 @@ static void check_batches() {
   CHECK(rc == ZO_OK && total == 40 && launches == 2, "huge batches: %zu segments in %zu launches", total, launches);
   // a launch failure stops the batching with its status
   launches = 0;
-  rc = plan_segments<kSegsPerLaunch>(segs.data(), (uint32_t)segs.size(), 2, 16, [&](const Plans<kSegsPerLaunch>&) {
+  rc = plan_segments<kSegsPerLaunch>(segs.data(), (uint32_t)segs.size(), 2, 16, 4, [&](const Plans<kSegsPerLaunch>&) {
     ++launches;
     return ZO_ERR_HIP;
   });

@@ -58,8 +58,8 @@ def test_calibration_library_exports_its_header():
     assert calib.zo_calib_rmw(None, 16, 1, None) == -1
     assert calib.zo_calib_rmw(ctypes.c_void_p(0x1008), 16, 1, None) == -2
     assert calib.zo_calib_rmw(ctypes.c_void_p(0x1000), 24, 1, None) == -2
-    assert calib.zo_calib_rmw_shape(None, 16, 1, 3, None) == -1
-    assert calib.zo_calib_rmw_shape(ctypes.c_void_p(0x1000), 16, 1, 4, None) == -2
+    assert calib.zo_calib_rmw_shape(None, 16, 1, 7, None) == -1
+    assert calib.zo_calib_rmw_shape(ctypes.c_void_p(0x1000), 16, 1, 8, None) == -2
     assert calib.zo_calib_rmw_shape(ctypes.c_void_p(0x1000), 1 << 41, 1, 0, None) == -2
 
 
