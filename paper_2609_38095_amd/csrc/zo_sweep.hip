@@ -385,12 +385,15 @@ __device__ __forceinline__ void tile_sums(float (&acc)[kTile], const float* tab,
   }
 }
 
-// theta + eps_r z_r - lr * sum, the restore of probe r merged with the update. A restore probe
-// inside the update's groups (r.eps != 0, RESTORE false) is folded into its group's table (see
-// build_tables). RESTORE: a restore probe outside them, applied per element as t =
+// How an update applies a restore probe r (theta + eps_r z_r - lr * sum, the restore merged
+// with the update): kNoRestore, none; kFolded, r lies in one of the update's probe groups and
+// is folded into that group's table (see build_tables), so the per-element work is the plain
+// update's; kPerElement, r lies outside them and is applied per element as t =
 // fl(theta + delta_r), then t minus the sum of the table values, its generator words made
 // after the group loop.
-template <class S, int NG, bool RESTORE, int N, int C, int BLOCK, int WPS, int PACE = 0, int AHEAD = 0>
+enum RestoreMode { kNoRestore = 0, kFolded = 1, kPerElement = 2 };
+
+template <class S, int NG, int RESTORE, int N, int C, int BLOCK, int WPS, int PACE = 0, int AHEAD = 0>
 __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uint32_t k_base, uint32_t K,
                                                       uint32_t n_groups, Coefs cf, float lr, Probe r) {
   // n_groups x 256 floats (C > 0: the interleaved copies): static for a fixed group count
@@ -400,7 +403,7 @@ __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uin
   float* tab = NG > 0 ? tab_fix : tab_dyn;
   const uint32_t g_first = k_base / 8;
   // the table a folded restore changes (none: a group index no table has; below g_first wraps)
-  const uint32_t fold_g = !RESTORE && r.eps != 0.0f ? r.group - g_first : 0xFFFFFFFFu;
+  const uint32_t fold_g = RESTORE == kFolded ? r.group - g_first : 0xFFFFFFFFu;
   // the tables are built while each wave's first loads are in flight (for_each_group's prologue)
   auto build = [&]() { build_tables<C, BLOCK>(tab, cf, k_base, K, n_groups, lr, fold_g, r); };
   // the lane's copy of a spread table (byte 0) and the second plane's offset (byte 2)
@@ -413,14 +416,14 @@ __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uin
     float acc[R][S::kVecElems];
     uint32_t Wr[R][S::kWords];  // the restore probe's words
     group_sums<S, NG, C>(acc, tab, gen, vbase, lane, n_groups, g_first, lane_off);
-    if (RESTORE) group_words(gen, vbase, lane, r.group, Wr, S());
+    if (RESTORE == kPerElement) group_words(gen, vbase, lane, r.group, Wr, S());
 #pragma unroll
     for (int u = 0; u < R; ++u) {
       float v[S::kVecElems];
       S::unpack(d[u], v);
 #pragma unroll
       for (int e = 0; e < S::kVecElems; ++e) {
-        if (RESTORE) v[e] = v[e] + delta(r, elem_byte<S>(Wr[u], e));
+        if (RESTORE == kPerElement) v[e] = v[e] + delta(r, elem_byte<S>(Wr[u], e));
         v[e] = v[e] - acc[u][e];
       }
       d[u] = S::pack(v);
@@ -429,10 +432,10 @@ __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uin
   for_each_edge<N, BLOCK>(ps, [&](const Plan& pl, uint64_t t) {
     float acc[kTile];
     tile_sums<C>(acc, tab, gen, t, n_groups, g_first);
-    const uint4 rr = RESTORE ? gen_block(gen, t, r.group) : make_uint4(0, 0, 0, 0);
+    const uint4 rr = RESTORE == kPerElement ? gen_block(gen, t, r.group) : make_uint4(0, 0, 0, 0);
     const uint32_t xr[4] = {rr.x, rr.y, rr.z, rr.w};
     tile_elementwise<S>(reinterpret_cast<typename S::storage*>(pl.base), pl.lo, pl.hi, t, [&](int e, float v) {
-      if (RESTORE) v = v + delta(r, word_byte(xr[e >> 2], e & 3));
+      if (RESTORE == kPerElement) v = v + delta(r, word_byte(xr[e >> 2], e & 3));
       return v - acc[e];
     });
   });
@@ -516,7 +519,7 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
   using C0 = integral_constant<int, 0>;
   // a restore probe outside the update's groups: the per-element restore, runtime group count
   if (w.restore && !w.fold) {
-    go(update_kernel<S, 0, true, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
+    go(update_kernel<S, 0, kPerElement, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
     return;
   }
   constexpr bool bf16 = sizeof(typename S::storage) == 2;
@@ -528,44 +531,52 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
   using C32 = integral_constant<int, 32>;
   // The tables and launch dimensions shape_for picks for each group count: streaming bf16
   // updates of two, four and eight groups take their own (two waves per stream; 1024-thread
-  // workgroups); everything else 256 threads. A folded restore runs these same kernels.
-  switch (w.n_groups) {
-    case 1:
-      if (copies)
-        go(update_kernel<S, 1, false, N, 32, kBlock, 1>, G1{}, C32{}, D256{});
-      else
-        go(update_kernel<S, 1, false, N, 0, kBlock, 1>, G1{}, C0{}, D256{});
-      break;
-    case 2:
-      if (!copies)
-        go(update_kernel<S, 2, false, N, 0, kBlock, 1>, G2{}, C0{}, D256{});
-      else if constexpr (!bf16)
-        go(update_kernel<S, 2, false, N, 32, kBlock, 1>, G2{}, C32{}, D256{});
-      else
-        go(update_kernel<S, 2, false, N, 32, 512, 2>, G2{}, C32{}, Dims<512, 2>{});
-      break;
-    case 4:
-      if constexpr (bf16) {
-        if (copies) {
-          go(update_kernel<S, 4, false, N, 32, 1024, 1>, G4{}, C32{}, Dims<1024, 1>{});
-          break;
+  // workgroups); everything else 256 threads. A folded restore runs the same code (its own
+  // instantiation, so that profiles tell the two calls apart).
+  auto dispatch = [&](auto mode) {
+    constexpr int M = decltype(mode)::value;
+    switch (w.n_groups) {
+      case 1:
+        if (copies)
+          go(update_kernel<S, 1, M, N, 32, kBlock, 1>, G1{}, C32{}, D256{});
+        else
+          go(update_kernel<S, 1, M, N, 0, kBlock, 1>, G1{}, C0{}, D256{});
+        break;
+      case 2:
+        if (!copies)
+          go(update_kernel<S, 2, M, N, 0, kBlock, 1>, G2{}, C0{}, D256{});
+        else if constexpr (!bf16)
+          go(update_kernel<S, 2, M, N, 32, kBlock, 1>, G2{}, C32{}, D256{});
+        else
+          go(update_kernel<S, 2, M, N, 32, 512, 2>, G2{}, C32{}, Dims<512, 2>{});
+        break;
+      case 4:
+        if constexpr (bf16) {
+          if (copies) {
+            go(update_kernel<S, 4, M, N, 32, 1024, 1>, G4{}, C32{}, Dims<1024, 1>{});
+            break;
+          }
         }
-      }
-      go(update_kernel<S, 4, false, N, 0, kBlock, 1>, G4{}, C0{}, D256{});
-      break;
-    case 8:
-      if constexpr (bf16) {
-        if (copies) {
-          go(update_kernel<S, 8, false, N, 16, 1024, 1>, G8{}, C16{}, Dims<1024, 1>{});
-          break;
+        go(update_kernel<S, 4, M, N, 0, kBlock, 1>, G4{}, C0{}, D256{});
+        break;
+      case 8:
+        if constexpr (bf16) {
+          if (copies) {
+            go(update_kernel<S, 8, M, N, 16, 1024, 1>, G8{}, C16{}, Dims<1024, 1>{});
+            break;
+          }
         }
-      }
-      go(update_kernel<S, 8, false, N, 0, kBlock, 1>, G8{}, C0{}, D256{});
-      break;
-    default:
-      go(update_kernel<S, 0, false, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
-      break;
-  }
+        go(update_kernel<S, 8, M, N, 0, kBlock, 1>, G8{}, C0{}, D256{});
+        break;
+      default:
+        go(update_kernel<S, 0, M, N, 0, kBlock, 1>, C0{}, C0{}, D256{});
+        break;
+    }
+  };
+  if (w.fold)
+    dispatch(integral_constant<int, kFolded>{});
+  else
+    dispatch(integral_constant<int, kNoRestore>{});
 }
 
 // One contiguous tensor.
