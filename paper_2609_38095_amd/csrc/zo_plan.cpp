@@ -114,9 +114,12 @@ Gen make_gen(uint64_t seed, uint32_t step) {
 // OPT-1.3B and Qwen3-8B (K = 60-64) and 3 G-element fp32 buffers:
 //   perturb, one or two probes: 256 threads, one workgroup per CU;
 //   update, one bf16 group: one workgroup per CU, one chunk per wave (OPT-30B K = 8: 6.19 ->
-//     6.53 TB/s);
+//     6.53 TB/s), paced at four outstanding memory operations as the perturb (+0.5%);
 //   update, two bf16 groups: 512 threads, two waves per stream, one chunk per stream, 32-copy
-//     tables (OPT-13B K = 16: +0.5 to 1.8%, +2% on a GPU already busy with perturbs);
+//     tables (OPT-13B K = 16: +0.5 to 1.8%, +2% on a GPU already busy with perturbs), paced
+//     at four outstanding memory operations (+0.3 to 0.5% on three boxes; 2, 3, 5, 6 and 8,
+//     three groups in flight, 16-copy tables, 256 threads and one wave per stream all equal
+//     or slower);
 //   update, three bf16 groups: three workgroups per CU, one group ahead;
 //   update, four bf16 groups: 1024 threads, 32-copy tables in two planes (OPT-30B K = 32:
 //     21.9 -> 21.6 ms);

@@ -531,8 +531,10 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
   using C32 = integral_constant<int, 32>;
   // The tables and launch dimensions shape_for picks for each group count: streaming bf16
   // updates of two, four and eight groups take their own (two waves per stream; 1024-thread
-  // workgroups); everything else 256 threads. A folded restore runs the same code (its own
-  // instantiation, so that profiles tell the two calls apart).
+  // workgroups); everything else 256 threads. bf16 updates of one and two groups are paced at
+  // four outstanding memory operations, as the one-probe perturb. A
+  // folded restore runs the same code (its own instantiation, so that profiles tell the two
+  // calls apart).
   auto dispatch = [&](auto mode) {
     constexpr int M = decltype(mode)::value;
     switch (w.n_groups) {
@@ -540,7 +542,7 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
         if (copies)
           go(update_kernel<S, 1, M, N, 32, kBlock, 1>, G1{}, C32{}, D256{});
         else
-          go(update_kernel<S, 1, M, N, 0, kBlock, 1>, G1{}, C0{}, D256{});
+          go(update_kernel<S, 1, M, N, 0, kBlock, 1, bf16 ? 4 : 0>, G1{}, C0{}, D256{});
         break;
       case 2:
         if (!copies)
@@ -548,7 +550,7 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
         else if constexpr (!bf16)
           go(update_kernel<S, 2, M, N, 32, kBlock, 1>, G2{}, C32{}, D256{});
         else
-          go(update_kernel<S, 2, M, N, 32, 512, 2>, G2{}, C32{}, Dims<512, 2>{});
+          go(update_kernel<S, 2, M, N, 32, 512, 2, 4>, G2{}, C32{}, Dims<512, 2>{});
         break;
       case 4:
         if constexpr (bf16) {
