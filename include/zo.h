@@ -115,8 +115,8 @@ int zo_probe_coeffs_ex(const double* L_plus, const double* L_minus, uint32_t K, 
  * eps = -fl(lr * c[0])) bit for bit.
  * Errors: ZO_ERR_NULL (params NULL with n > 0, c NULL with K > 0), ZO_ERR_ARG (dtype,
  * alignment, K > ZO_K_MAX, k_base + K > 2^32), ZO_ERR_NONFINITE (lr or any c[k]), ZO_ERR_HIP.
- * Cost: one read and one write of theta; above about 24 probes (bf16) the sweep is bound by
- * the probe generator (VALU) and the LDS table lookups rather than by HBM.
+ * Cost: one read and one write of theta; above about 16 probes (bf16) the sweep is bound by
+ * the probe generator and the table arithmetic (VALU) rather than by HBM.
  */
 int zo_update(void* params, zo_dtype dtype, uint64_t n, uint64_t seed, uint32_t step,
               uint32_t K, const float* c, float lr, void* stream);
