@@ -488,15 +488,15 @@ void launch_sweep(const Plans<N>& ps, const Gen& gen, const Sweep& w, const Shap
       kernel<<<grid_of(kBlock, 1), dim3(kBlock), pad, st>>>(ps, gen, w.a, b);
     };
     // paced when the generator work per byte is lightest: one probe group, or fp32 with two;
-    // bf16 at 4 outstanding operations (one probe +1.3%, two in one group +3.4% over 2), fp32
-    // at 2 (4 measured equal or lower)
-    constexpr int kPace = sizeof(typename S::storage) == 2 ? 4 : 2;
+    // at 4 outstanding operations (bf16: one probe +1.3%, two in one group +3.4% over 2; fp32
+    // one probe +3%), the fp32 two-probe perturb at 2 (4 measured equal or lower)
+    constexpr int kPace2 = sizeof(typename S::storage) == 2 ? 4 : 2;
     const bool two_groups = w.two && w.a.group != w.b.group;
     const bool paced = (two_groups ? 2u : 1u) * (sizeof(typename S::storage) == 2 ? 2u : 1u) <= 2u;
     if (w.two)
-      paced ? go(perturb_kernel<S, true, N, kPace, kBlock, 1>, w.b) : go(perturb_kernel<S, true, N, 0, kBlock, 1>, w.b);
+      paced ? go(perturb_kernel<S, true, N, kPace2, kBlock, 1>, w.b) : go(perturb_kernel<S, true, N, 0, kBlock, 1>, w.b);
     else
-      paced ? go(perturb_kernel<S, false, N, kPace, kBlock, 1>, w.a) : go(perturb_kernel<S, false, N, 0, kBlock, 1>, w.a);
+      paced ? go(perturb_kernel<S, false, N, 4, kBlock, 1>, w.a) : go(perturb_kernel<S, false, N, 0, kBlock, 1>, w.a);
     return;
   }
   const uint32_t copies = sh.copies;
@@ -617,7 +617,11 @@ int run_segments(const zo_segment* segs, uint32_t n_segs, uint64_t seed, uint32_
   hipStream_t st = static_cast<hipStream_t>(stream);
   uint64_t total = 0;  // the call's weights decide the streaming shape of all its launches
   for (uint32_t i = 0; i < n_segs; ++i) total += segs[i].n;
-  const Shape sh = shape_for(total, sizeof(typename S::storage), w);
+  Shape sh = shape_for(total, sizeof(typename S::storage), w);
+  // at most one chunk per stream: a tensor boundary then idles at most one chunk slot per
+  // stream of a workgroup (Qwen3-8B as 399 tensors, K = 60: update 10.4-10.5 -> 9.8-9.9 ms
+  // against four chunks per stream)
+  if (sh.chunks_per_wave > 1) sh.chunks_per_wave = 1;
   (void)hipGetLastError();
   return plan_segments<kSegsPerLaunch>(segs, n_segs, sizeof(typename S::storage), sh.chunk_groups,
                                        streams_per_block(sh), [&](const Plans<kSegsPerLaunch>& ps) {
