@@ -160,12 +160,13 @@ __device__ __forceinline__ void store_group(char* base, const u32x4 (&d)[GroupSh
 // its next AHEAD groups in flight while the body works on the current one (a stream of up to
 // 32 KiB, reads and writes interleaved). More waves per stream give the generator and table
 // work more waves to hide behind without adding streams. A wave's chunk indices increase,
-// so its segment cursor only moves forward. PACE > 0 (two ahead only): each step of three
-// groups first waits until at most PACE memory operations of the wave are outstanding: with
-// 2, only the step's own prefetch; with 4, also the previous step's last stores. The
-// lightest sweeps stream HBM faster paced (OPT-13B bf16 perturb: 6.40 TB/s with every
-// request the loop allows in flight, 6.67 paced at 2, 6.76 at 4; pacing at 6 or 8 measured
-// lower), heavier ones need the overlap.
+// so its segment cursor only moves forward. PACE > 0 (two or three ahead): each step of
+// the loop first waits until at most PACE memory operations of the wave are outstanding:
+// two ahead, with 2 only the step's own prefetch, with 4 also the previous step's last
+// stores. The lighter sweeps stream HBM faster paced (OPT-13B bf16 perturb: 6.40 TB/s with
+// every request the loop allows in flight, 6.67 paced at 2, 6.76 at 4; pacing at 6 or 8
+// measured lower; the one- and two-group bf16 updates +0.3-0.5% at 4), heavier ones need the
+// overlap.
 // prologue() runs once per wave, after the loads of the wave's first group are issued (at
 // once for a wave without groups), so that work such as building the update's LDS tables
 // overlaps their latency; it may hold a workgroup barrier, which every wave reaches once.

@@ -16,8 +16,9 @@
 //
 // zo_perturb_segments / zo_update_segments sweep a list of separate tensors: the host validates
 // the list, builds one plan per tensor and launches batches of up to 64 plans (kernel
-// arguments); inside a launch the chunks and edge tiles of all its tensors are numbered
-// consecutively and each wave finds its chunk's tensor by a binary search.
+// arguments); inside a launch the chunk slots and edge tiles of all its tensors are numbered
+// consecutively (slots aligned to memory, zo_plan.h) and each wave finds its chunk's tensor
+// by a binary search.
 //
 // The update keeps, per probe group, a 256-entry table in LDS: entry b is lr times the signed
 // sum of the group's 8 coefficients selected by the bits of b (pairwise), so applying 8 probes
@@ -409,8 +410,8 @@ __global__ __launch_bounds__(BLOCK) void update_kernel(Plans<N> ps, Gen gen, uin
   // the lane's copy of a spread table (byte 0) and the second plane's offset (byte 2)
   const uint32_t lane_off = 4u * (threadIdx.x % (C > 0 ? C : 32)) | (1u << 16);
   constexpr int R = GroupShape<S>::kRows;
-  // two groups in flight for the table counts that stream at one or two workgroups per CU;
-  // one for the heavier updates, which run more waves per CU (AHEAD > 0 sets it)
+  // two groups in flight with spread tables and for one, two or four groups; one for the
+  // other counts, which run at three or more workgroups per CU (AHEAD > 0 sets it)
   constexpr int kAhead = AHEAD ? AHEAD : C > 0 || NG == 1 || NG == 2 || NG == 4 ? 2 : 1;
   for_each_group<S, kAhead, N, PACE, BLOCK, WPS>(ps, [&](uint64_t vbase, u32x4 (&d)[R], uint32_t lane) {
     float acc[R][S::kVecElems];
