@@ -25,6 +25,8 @@
  *   - stream: a hipStream_t (NULL = the default stream). Device work is enqueued on it
  *     and the call returns without waiting; faults surface at the caller's next
  *     synchronisation. Host arguments (coefficient arrays) are copied before return.
+ *   - device: params (every segment's) and stream belong to the calling thread's current
+ *     HIP device, on which the kernels are launched.
  *   - Errors: every argument is validated before anything is launched; on ZO_ERR_NULL,
  *     ZO_ERR_ARG or ZO_ERR_NONFINITE nothing was enqueued and no output was written.
  *     ZO_ERR_HIP reports a launch the runtime refused (for the segment calls, earlier

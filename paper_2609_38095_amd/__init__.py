@@ -102,9 +102,12 @@ def _check(status, what):
 
 def _stream(theta_or_device, stream):
     """The hipStream_t to launch on: torch's current stream of the tensor's device, or the
-    given stream (a torch stream, which must belong to that device, or a raw handle)."""
+    given stream (a torch stream, which must belong to that device, or a raw handle). The
+    library launches on the current device, so the tensors must live there."""
     import torch
     dev = theta_or_device.device if hasattr(theta_or_device, "device") else theta_or_device  # None: no tensors
+    if dev is not None and torch.device(dev).index not in (None, torch.cuda.current_device()):
+        raise ValueError(f"the tensors live on {dev}, the current device is cuda:{torch.cuda.current_device()}")
     if stream is None:
         return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
     if hasattr(stream, "cuda_stream"):
