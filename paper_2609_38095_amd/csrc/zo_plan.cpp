@@ -131,7 +131,8 @@ Gen make_gen(uint64_t seed, uint32_t step) {
 // update with that group's table changed, and takes the update's shape. Other updates (five to
 // seven bf16 groups, more than eight, or more than six in fp32, and a restore probe outside
 // the update's groups) are bound by the generator or the LDS table lookups and keep 4 KiB
-// chunks at full occupancy, as do sweeps smaller than the 256 MiB Infinity Cache. Grids: up to
+// chunks at full occupancy, as do perturbs smaller than the 256 MiB Infinity Cache (updates
+// of such buffers take 8 KiB chunks at full occupancy). Grids: up to
 // kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of many short-lived
 // workgroups keeps the streams compact; a persistent grid of one workgroup per CU measured
 // 5.6 TB/s), except where a number of chunks per stream is given: the one-probe bf16 perturb,
@@ -141,7 +142,13 @@ Gen make_gen(uint64_t seed, uint32_t step) {
 Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   const uint64_t group_bytes = kGroupElems * elem;
   const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0, 0};
-  if (elements * elem < kStreamBytes) return short_chunks;
+  if (elements * elem < kStreamBytes) {
+    if (!w.update) return short_chunks;
+    // updates of cache-sized buffers: 8 KiB chunks, so that each workgroup's table build
+    // serves twice the bytes (OPT-125M: K = 16 0.088 -> 0.084 ms, K = 60 0.201 -> 0.189 ms;
+    // 16 and 32 KiB chunks measured slower at K = 16)
+    return Shape{static_cast<uint32_t>(8192 / group_bytes), 0, 0};
+  }
   const uint32_t chunk = static_cast<uint32_t>(kMaxChunkBytes / group_bytes);
   if (!w.update) {
     const bool one_probe_bf16 = !w.two && elem == 2, two_probes_fp32 = w.two && elem == 4;
