@@ -135,10 +135,11 @@ Gen make_gen(uint64_t seed, uint32_t step) {
 // of such buffers take 8 KiB chunks at full occupancy). Grids: up to
 // kDefaultMaxBlocks workgroups, grid-stride beyond (in-order dispatch of many short-lived
 // workgroups keeps the streams compact; a persistent grid of one workgroup per CU measured
-// 5.6 TB/s), except where a number of chunks per stream is given: the one-probe bf16 perturb,
-// the two-probe fp32 perturb and the bf16 updates of one or two groups run one chunk per stream
-// (OPT-13B: the perturb 6.48 -> 6.67 TB/s, OPT-30B 6.20 -> 6.60; 3 G fp32 weights: the
-// two-probe perturb 6.30 -> 6.48 across two probe groups).
+// 5.6 TB/s), except where a number of chunks per stream is given: the bf16 perturb of one
+// probe or of two in one probe group, the two-probe fp32 perturb and the bf16 updates of one
+// or two groups run one chunk per stream (OPT-13B: the perturb 6.48 -> 6.67 TB/s, OPT-30B
+// 6.20 -> 6.60; two probes in one group +1%, across two groups -0.3%, so those stay
+// grid-stride; 3 G fp32 weights: the two-probe perturb 6.30 -> 6.48 across two probe groups).
 Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   const uint64_t group_bytes = kGroupElems * elem;
   const Shape short_chunks{static_cast<uint32_t>(4096 / group_bytes ? 4096 / group_bytes : 1), 0, 0};
@@ -151,8 +152,10 @@ Shape shape_for(uint64_t elements, size_t elem, const Sweep& w) {
   }
   const uint32_t chunk = static_cast<uint32_t>(kMaxChunkBytes / group_bytes);
   if (!w.update) {
-    const bool one_probe_bf16 = !w.two && elem == 2, two_probes_fp32 = w.two && elem == 4;
-    return Shape{chunk, 1, one_probe_bf16 || two_probes_fp32 ? 1u : 0u};
+    // one chunk per wave: bf16 with one probe or two in one group, fp32 with two probes
+    const bool one_group_bf16 = elem == 2 && (!w.two || w.a.group == w.b.group);
+    const bool two_probes_fp32 = w.two && elem == 4;
+    return Shape{chunk, 1, one_group_bf16 || two_probes_fp32 ? 1u : 0u};
   }
   if (w.restore && !w.fold) return short_chunks;
   const uint32_t g = w.n_groups;
